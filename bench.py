@@ -1,0 +1,214 @@
+#!/usr/bin/env python3
+"""Benchmark of the exit-head training step (EE-Tuning) on one MI355X.
+
+A step is one ee_multi_exit_step over one synthetic batch: for every exit,
+forward (norm, optional SwiGLU MLP, vocabulary projection, cross-entropy),
+backward into the exit's own parameters, weighted loss.  Inputs are resident
+in HBM before the timed region starts.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "exit-head fwd+bwd tokens/sec at h=4096,V=32000; % bf16 MFMA peak"
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense MFMA
+PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_flops(w, name):
+    """Algorithmic flops of one launch of each GEMM of the step (2 per MAC)."""
+    N, h, V, I = w.n_tokens, w.hidden, w.vocab, w.intermediate
+    table = {
+        "logits + softmax partials": 2 * N * h * V,
+        "output-matrix gradient": 2 * N * h * V,
+        "gate projection": 2 * N * h * I,
+        "up projection + swiglu": 2 * N * h * I,
+        "down projection + residual": 2 * N * h * I,
+        "dZ": 2 * N * h * V,
+        "dA + swiglu backward": 2 * N * h * I,
+        "down gradient": 2 * N * h * I,
+        "gate gradient": 2 * N * h * I,
+        "up gradient": 2 * N * h * I,
+    }
+    return table.get(name)
+
+
+def step_flops(w):
+    """Algorithmic flops per step: 4hV per token per Norm/Embedding exit and
+    14hI + 6hV per token per MLP exit (the gain gradients come from the
+    weight-gradient GEMMs, so no dU product is needed)."""
+    N, h, V, I = w.n_tokens, w.hidden, w.vocab, w.intermediate
+    per = 14 * h * I + 6 * h * V if w.kind == 2 else 4 * h * V
+    return per * N * w.n_exits
+
+
+def source_digest():
+    d = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2402_00518_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".h", ".hip", ".cpp")):
+            d.update(open(os.path.join(csrc, f), "rb").read())
+    return d.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources; else None."""
+    try:
+        data = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    rec = data.get(workload, {}).get(kernel)
+    if not rec or rec.get("source_digest") != source_digest():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(batch, sample_tokens):
+    import numpy as np
+    import oracle as O
+    import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((p.get("num_threads", 1) for p in threadpool_info()
+                       if p.get("user_api") == "blas"), default=1)
+    except Exception:
+        threads = 1
+    w = batch.workload
+    n = min(sample_tokens, w.n_tokens)
+    exits = O.exits_from_batch(batch)
+    xs = [W.decode(x[:n]) for x in batch.hidden]
+    y = batch.targets[:n]
+    t0 = time.perf_counter()
+    O.multi_exit_step(exits, xs, y, list(w.exit_weights))
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n} of {w.n_tokens} tokens, all {w.n_exits} exit(s), full h={w.hidden} "
+                      f"V={w.vocab}; fp64 numpy forward+backward, {dt:.1f} s",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama7b_norm")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=512)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-pass", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs the exit-head step on one GPU only; --gpus {args.gpus} "
+              "is not supported (how the step would shard is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    from paper_2402_00518_amd import binding as B
+    from paper_2402_00518_amd.session import Session
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    B.lib()
+    w = W.WORKLOADS[args.workload]
+    log(f"workload {w.name}: N={w.n_tokens} h={w.hidden} V={w.vocab} I={w.intermediate} "
+        f"exits={w.n_exits} {w.dtype}")
+    t0 = time.time()
+    batch = W.make_batch(w, args.seed)
+    sess = Session.from_batch(batch)
+    torch.cuda.synchronize()
+    log(f"inputs generated and resident in HBM ({time.time() - t0:.1f} s)")
+
+    for _ in range(args.warmup):
+        sess.step()
+    torch.cuda.synchronize()
+    sess.check_device_error()
+    log(f"warmup {args.warmup} steps done, loss {sess.loss_total.item():.5f}")
+
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        sess.step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    loss = sess.loss_total.item()
+    log(f"timed {args.steps} steps: {ms:.4f} ms/step, loss {loss:.5f}")
+
+    flops = step_flops(w)
+    peak = PEAK_TFLOPS[w.dtype]
+    tokens_per_s = w.n_tokens / (ms / 1e3)
+    out = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "kind": ["embedding", "norm", "mlp"][w.kind],
+                   "n_tokens": w.n_tokens, "hidden": w.hidden, "vocab": w.vocab,
+                   "intermediate": w.intermediate, "exits": w.n_exits,
+                   "exit_weights": list(w.exit_weights)},
+        "mfma_peak_frac": flops / (ms / 1e3) / (peak * 1e12),
+        "step_tflops": flops / (ms / 1e3) / 1e12,
+        "loss": loss,
+    }
+
+    if not args.no_kernel_pass:
+        B.ee_profile_start()
+        for _ in range(args.steps):
+            sess.step()
+        kt = B.ee_profile_stop()
+        kernels = {k: {"launches": n, "avg_ms": t / n} for k, (n, t) in kt.items()}
+        out["kernels"] = kernels
+        dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
+        f = kernel_flops(w, dom)
+        avg_s = kernels[dom]["avg_ms"] / 1e3
+        if f is not None:
+            ach = f / avg_s / 1e12
+            out["roofline"] = {"bound": "mfma", "kernel": dom, "achieved": ach, "peak": peak,
+                               "unit": "TFLOP/s", "frac": ach / peak,
+                               "traffic": measured_traffic(w.name, dom),
+                               "flops_per_launch": f, "avg_ms": kernels[dom]["avg_ms"]}
+        log(f"dominant kernel {dom}: {kernels[dom]['avg_ms']:.4f} ms")
+
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle on {args.cpu_sample_tokens} tokens ...")
+        out["cpu_baseline"] = cpu_baseline(batch, args.cpu_sample_tokens)
+        log(f"cpu baseline {out['cpu_baseline']['value']:.1f} tokens/s")
+
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,212 @@
+/*
+ * ee_tuning.h -- C ABI of the MI355X (gfx950) early-exit head training step.
+ *
+ * EE-Tuning (arXiv 2402.00518) converts a frozen pre-trained LLM into an
+ * early-exit one by attaching exit heads to intermediate hidden states and
+ * tuning only those heads.  This library runs the hot part of one tuning
+ * iteration (Sec. 3.2, "Computational efficiency", item 2): for every exit,
+ * the forward pass, the next-token loss, and the backward pass into the
+ * exit's own parameters.  The backbone is frozen, so no gradient is produced
+ * for the hidden states (Sec. 3.2, first paragraph).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Device pointers are HIP device addresses on the current device; host
+ *    pointers are marked "host".  Every device pointer must be 16-byte
+ *    aligned.  The caller owns all memory; the library allocates nothing per
+ *    call and keeps no state besides its loaded kernels and a thread-local
+ *    error string.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued
+ *    asynchronously on it; scalars written to device memory are valid once
+ *    the stream has been synchronised.
+ *  - Every error that the host can detect (NULL pointers, bad shapes, bad
+ *    dtype, misalignment, small workspace, aliased outputs, unsupported exit
+ *    kind) is reported before anything is enqueued: nothing runs.  A detail
+ *    string is then available from ee_last_error().
+ *  - Targets outside [0, V) are a precondition violation that only the
+ *    device sees: the kernels never access memory with them, record the
+ *    fault in the workspace, and ee_check_device_error() reports it.
+ *  - Matrices are row-major.  The output embedding, an h x V matrix in the
+ *    paper (Sec. 3.1, Embedding exit), is stored as W_out[V][h], the common
+ *    checkpoint layout; it is the same matrix.
+ *  - Mixed precision (EE_BF16): hidden states and weights are bf16; norms,
+ *    softmax and losses run in fp32; GEMMs take bf16 operands with fp32
+ *    accumulation; weight gradients are written in fp32.  EE_F32 keeps every
+ *    operand in fp32.
+ */
+#ifndef EE_TUNING_H
+#define EE_TUNING_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EE_ABI_VERSION 1
+
+typedef enum ee_status {
+  EE_OK = 0,
+  EE_ERR_NULL = 1,        /* a required pointer is NULL                       */
+  EE_ERR_SHAPE = 2,       /* a size is out of range or not a multiple of 64   */
+  EE_ERR_DTYPE = 3,       /* unknown dtype, or dtypes of exits disagree       */
+  EE_ERR_ALIGN = 4,       /* a device pointer is not 16-byte aligned          */
+  EE_ERR_WORKSPACE = 5,   /* workspace smaller than ee_workspace_bytes()      */
+  EE_ERR_ALIAS = 6,       /* an output overlaps another output or an input    */
+  EE_ERR_UNSUPPORTED = 7, /* exit kind or flag not implemented (Layer exit)   */
+  EE_ERR_TARGET = 8,      /* device saw a target outside [0, V)               */
+  EE_ERR_HIP = 9          /* a HIP runtime call or launch failed              */
+} ee_status;
+
+typedef enum ee_dtype { EE_F32 = 0, EE_BF16 = 1 } ee_dtype;
+
+/* Exit architectures of Sec. 3.1 ("Architectures of early exits"):
+ *  EMBEDDING  logits = X W_out^T                                  (one matrix)
+ *  NORM       logits = RMSNorm_gamma(X) W_out^T       (RMSNorm as in Sec. 4.2)
+ *  MLP        Y = X + SwiGLU(RMSNorm_gamma_mlp(X)) W_down^T   (pre-norm residual
+ *             module, Fig. 2 caption), logits = RMSNorm_gamma(Y) W_out^T
+ *  LAYER      a full Transformer layer in front of Norm: EE_ERR_UNSUPPORTED.
+ * RMSNorm: s_hat = s (mean_j s_j^2 + eps)^(-1/2), then times the gain.
+ * SwiGLU:  A = silu(U W_gate^T) * (U W_up^T), silu(t) = t / (1 + exp(-t)). */
+typedef enum ee_exit_kind {
+  EE_EXIT_EMBEDDING = 0,
+  EE_EXIT_NORM = 1,
+  EE_EXIT_MLP = 2,
+  EE_EXIT_LAYER = 3
+} ee_exit_kind;
+
+/* Step flags. */
+#define EE_FLAG_DYNAMIC_TOKEN_WEIGHTS 1u
+/* Appendix "Dynamic token-wise loss weighting": weight each token's NLL by
+ * its detached confidence c_n = max_v softmax(S[n, :]).  Multiplies any
+ * caller token weights. */
+
+/* One exit's parameters (read-only; may alias another exit's, e.g. after
+ * the "copy" initialisation of Sec. 3.1). */
+typedef struct ee_exit {
+  int32_t kind;          /* ee_exit_kind                                     */
+  int32_t dtype;         /* ee_dtype of the hidden states and all weights    */
+  int64_t hidden;        /* h: multiple of 64, 64 <= h <= 32768              */
+  int64_t vocab;         /* V: 1 <= V <= 1048576                             */
+  int64_t intermediate;  /* I (MLP only): multiple of 64, <= 65536; else 0   */
+  float rms_eps;         /* RMSNorm epsilon, >= 0 (Llama-2 uses 1e-5)        */
+  int32_t reserved;      /* must be 0                                        */
+  const void *w_out;     /* [V][h]                                           */
+  const void *gamma;     /* [h] exit RMSNorm gain (NORM, MLP)                */
+  const void *gamma_mlp; /* [h] MLP pre-norm gain (MLP)                      */
+  const void *w_gate;    /* [I][h] (MLP)                                     */
+  const void *w_up;      /* [I][h] (MLP)                                     */
+  const void *w_down;    /* [h][I] (MLP)                                     */
+} ee_exit;
+
+/* Gradients of one exit's parameters, fp32, same shapes as the parameters.
+ * Pointers for parameters the exit kind does not have are ignored. */
+typedef struct ee_exit_grads {
+  float *d_w_out;
+  float *d_gamma;
+  float *d_gamma_mlp;
+  float *d_w_gate;
+  float *d_w_up;
+  float *d_w_down;
+} ee_exit_grads;
+
+/* Bytes of device workspace needed to run the given exits over n_tokens
+ * rows, forward and backward.  One workspace serves every exit of
+ * ee_multi_exit_step (they run one after another on the stream).  Returns 0
+ * if the arguments are invalid (ee_last_error() says why). */
+size_t ee_workspace_bytes(int n_exits, const ee_exit *exits, int64_t n_tokens);
+
+/* Forward pass and loss of one exit (Sec. 2 loss; Sec. 3.1 architectures).
+ *
+ *   L_e = (1/N) sum_n m_n * ( logsumexp_v S[n, v] - S[n, y_n] ),
+ *   S   = exit(hidden) W_out^T,
+ *
+ * with m_n = token_w[n] (all ones when token_w is NULL), times the detached
+ * confidence with EE_FLAG_DYNAMIC_TOKEN_WEIGHTS.  The mean over the N rows
+ * reads the paper's sum over tokens as a per-token average.
+ *
+ *   hidden    device [N][h], dtype of the exit: the frozen backbone's hidden
+ *             states at this exit; row n predicts targets[n] (already
+ *             shifted by one position).
+ *   targets   device [N] int32 token ids in [0, V).
+ *   token_w   device [N] fp32, or NULL.
+ *   exit_weight  w_e, scales the gradients that ee_head_backward produces.
+ *   loss      device [1] fp32: L_e (not multiplied by w_e).
+ *   row_loss  device [N] fp32 per-row NLL, or NULL.
+ *   ws        device workspace of ws_bytes >= ee_workspace_bytes(1, e, N).
+ *
+ * Leaves in ws everything ee_head_backward needs, including the logit
+ * gradient seed w_e m_n / N * (softmax(S[n]) - onehot(y_n)).  The workspace
+ * must not be touched between the two calls. */
+ee_status ee_head_forward_loss(const ee_exit *e, const void *hidden,
+                               const int32_t *targets, const float *token_w,
+                               int64_t n_tokens, float exit_weight,
+                               uint32_t flags, void *ws, size_t ws_bytes,
+                               float *loss, float *row_loss, void *stream);
+
+/* Backward pass of one exit into its own parameters only (Sec. 3.2): writes
+ * w_e * dL_e/dtheta_e for every parameter of the exit kind, consuming the
+ * workspace a preceding ee_head_forward_loss left for the same exit and N.
+ * accumulate = 0 overwrites the gradient buffers, 1 adds to them. */
+ee_status ee_head_backward(const ee_exit *e, int64_t n_tokens, void *ws,
+                           size_t ws_bytes, const ee_exit_grads *g,
+                           int accumulate, void *stream);
+
+/* One full step over all exits (Sec. 3.2: exits are tuned independently and
+ * their losses combine as a weighted sum, Sec. 1):
+ *
+ *   L = sum_e exit_weights[e] * L_e,
+ *
+ * equal to ee_head_forward_loss + ee_head_backward for each exit in turn.
+ * All exits share N, V, targets, token_w and flags; each has its own hidden
+ * states hidden[e] (device pointers in a host array) and parameters.
+ *   exit_weights   host [n_exits]
+ *   grads          host [n_exits] gradient buffer sets
+ *   loss_total     device [1];  loss_per_exit device [n_exits] or NULL. */
+ee_status ee_multi_exit_step(int n_exits, const ee_exit *exits,
+                             const void *const *hidden, const int32_t *targets,
+                             const float *token_w, int64_t n_tokens,
+                             const float *exit_weights, uint32_t flags,
+                             const ee_exit_grads *grads, int accumulate,
+                             void *ws, size_t ws_bytes, float *loss_total,
+                             float *loss_per_exit, void *stream);
+
+/* Synchronises `stream`, then reports EE_ERR_TARGET if the latest
+ * ee_head_forward_loss or ee_multi_exit_step call on this workspace saw a
+ * target outside [0, V) (each such call starts with a clean record), and
+ * clears the record.  EE_OK otherwise. */
+ee_status ee_check_device_error(void *ws, size_t ws_bytes, void *stream);
+
+/* Kernel timing, for diagnostics.  Between ee_profile_start() and
+ * ee_profile_stop(), every kernel the step functions launch is bracketed by a
+ * pair of HIP events recorded on the launch stream (the events cost a few
+ * microseconds per launch; keep them out of headline timings).
+ * ee_profile_stop() waits for the recorded events, fills up to `capacity`
+ * entries of `out` (host array) with per-kernel launch counts and summed
+ * durations, in first-launch order, and returns the number of entries, or -1
+ * on a HIP error.  Names are static strings owned by the library.  Process-
+ * wide; not meant for concurrent use from several threads. */
+typedef struct ee_kernel_time {
+  const char *name;
+  int32_t launches;
+  double total_ms;
+} ee_kernel_time;
+
+ee_status ee_profile_start(void);
+int ee_profile_stop(ee_kernel_time *out, int capacity);
+
+/* Static description of a status code. */
+const char *ee_status_string(ee_status s);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char *ee_last_error(void);
+
+/* EE_ABI_VERSION of the loaded library. */
+int ee_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EE_TUNING_H */

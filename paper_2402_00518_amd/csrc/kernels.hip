@@ -1,0 +1,441 @@
+// Exit-head kernels for gfx950: RMSNorm forward/backward, the cross-entropy
+// reduction and seed, the loss and gain-gradient reductions, and the GEMM
+// instantiations with their fused epilogues.
+#include <math.h>
+
+#include "epilogues.h"
+#include "launch.h"
+
+namespace ee {
+
+// ------------------------------------------------------------ vector I/O
+template <typename T, int N> __device__ __forceinline__ void load_f32(const T *p, float (&out)[N]);
+
+template <int N> __device__ __forceinline__ void load_f32(const float *p, float (&out)[N]) {
+  static_assert(N % 4 == 0, "");
+#pragma unroll
+  for (int c = 0; c < N / 4; ++c) {
+    const f32x4_t v = reinterpret_cast<const f32x4_t *>(p)[c];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) out[c * 4 + e] = v[e];
+  }
+}
+
+template <int N> __device__ __forceinline__ void load_f32(const bf16_t *p, float (&out)[N]) {
+  static_assert(N % 4 == 0, "");
+  if constexpr (N % 8 == 0) {
+#pragma unroll
+    for (int c = 0; c < N / 8; ++c) {
+      const u32x4_t w = reinterpret_cast<const u32x4_t *>(p)[c];
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        out[c * 8 + 2 * d] = __uint_as_float(w[d] << 16);
+        out[c * 8 + 2 * d + 1] = __uint_as_float(w[d] & 0xFFFF0000u);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < N / 4; ++c) {
+      const u32x2_t w = reinterpret_cast<const u32x2_t *>(p)[c];
+#pragma unroll
+      for (int d = 0; d < 2; ++d) {
+        out[c * 4 + 2 * d] = __uint_as_float(w[d] << 16);
+        out[c * 4 + 2 * d + 1] = __uint_as_float(w[d] & 0xFFFF0000u);
+      }
+    }
+  }
+}
+
+template <int N> __device__ __forceinline__ void store_f32(float *p, const float (&in)[N]) {
+#pragma unroll
+  for (int c = 0; c < N / 4; ++c)
+    reinterpret_cast<f32x4_t *>(p)[c] = f32x4_t{in[c * 4], in[c * 4 + 1], in[c * 4 + 2], in[c * 4 + 3]};
+}
+
+template <int N> __device__ __forceinline__ void store_f32(bf16_t *p, const float (&in)[N]) {
+  static_assert(N % 8 == 0, "");
+#pragma unroll
+  for (int c = 0; c < N / 8; ++c) {
+    u32x4_t w;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      w[d] = static_cast<uint32_t>(f32_to_bf16(in[c * 8 + 2 * d])) |
+             (static_cast<uint32_t>(f32_to_bf16(in[c * 8 + 2 * d + 1])) << 16);
+    reinterpret_cast<u32x4_t *>(p)[c] = w;
+  }
+}
+
+// -------------------------------------------------------------- RMSNorm
+// One wave per row; fp32 sum of squares reduced across the wave.
+template <typename Tin>
+__global__ __launch_bounds__(256) void row_rms_kernel(const Tin *x, int64_t ldx, int n, int h, float eps,
+                                                      float *r) {
+  constexpr int V = 16 / sizeof(Tin);
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const Tin *xr = x + static_cast<int64_t>(row) * ldx;
+  float s = 0.0f;
+  for (int j = lane * V; j < h; j += kWave * V) {
+    float v[V];
+    load_f32<V>(xr + j, v);
+#pragma unroll
+    for (int e = 0; e < V; ++e) s += v[e] * v[e];
+  }
+  s = warp_sum(s);
+  if (lane == 0) r[row] = 1.0f / sqrtf(s / static_cast<float>(h) + eps);
+}
+
+// 64 tokens x 64 features per block.  Row-major outputs are written
+// directly; the token-contiguous copy of x_hat goes through an LDS
+// transpose so that both sides are coalesced.
+template <typename Tin, typename T>
+__global__ __launch_bounds__(256) void norm_apply_kernel(const Tin *x, int64_t ldx, const float *r,
+                                                         const T *gain, int n, int ldn, int h, T *z,
+                                                         T *x_hat, T *x_hat_t) {
+  __shared__ float tile[64][65];
+  const int n0 = blockIdx.x * 64, j0 = blockIdx.y * 64;
+  const int tid = threadIdx.x;
+  const int tr = tid >> 2, tc = (tid & 3) * 16;
+  const int row = n0 + tr;
+  float v[16];
+  if (row < n) {
+    load_f32<16>(x + static_cast<int64_t>(row) * ldx + j0 + tc, v);
+    const float rs = r != nullptr ? r[row] : 1.0f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) v[e] *= rs;
+    const int64_t o = static_cast<int64_t>(row) * h + j0 + tc;
+    if (x_hat != nullptr) store_f32<16>(x_hat + o, v);
+    if (z != nullptr) {
+      float zz[16];
+      if (gain != nullptr) {
+        float g[16];
+        load_f32<16>(gain + j0 + tc, g);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) zz[e] = v[e] * g[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) zz[e] = v[e];
+      }
+      store_f32<16>(z + o, zz);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) v[e] = 0.0f;
+  }
+  if (x_hat_t == nullptr) return;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) tile[tr][tc + e] = v[e];
+  __syncthreads();
+  const int fr = tid >> 2, tk = (tid & 3) * 16;
+  float o[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) o[e] = tile[tk + e][fr];
+  store_f32<16>(x_hat_t + static_cast<int64_t>(j0 + fr) * ldn + n0 + tk, o);
+}
+
+// RMSNorm backward, one wave per row (see launch.h for the formula).
+template <typename T>
+__global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, const float *y, const float *r,
+                                                       const T *gain, int n, int h, T *dy) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= n) return;
+  const int64_t o = static_cast<int64_t>(row) * h;
+  const float rr = r[row];
+  float s = 0.0f;
+  for (int j = lane * 8; j < h; j += kWave * 8) {
+    float a[8], b[8], g[8];
+    load_f32<8>(dz + o + j, a);
+    load_f32<8>(y + o + j, b);
+    load_f32<8>(gain + j, g);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s += a[e] * g[e] * b[e] * rr;
+  }
+  const float proj = warp_sum(s) / static_cast<float>(h);
+  for (int j = lane * 8; j < h; j += kWave * 8) {
+    float a[8], b[8], g[8], d[8];
+    load_f32<8>(dz + o + j, a);
+    load_f32<8>(y + o + j, b);
+    load_f32<8>(gain + j, g);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) d[e] = rr * (a[e] * g[e] - b[e] * rr * proj);
+    store_f32<8>(dy + o + j, d);
+  }
+}
+
+// ---------------------------------------------------------- cross-entropy
+__global__ __launch_bounds__(256) void ce_reduce_kernel(CeReduceArgs a) {
+  __shared__ float red[256];
+  const int n = blockIdx.x * 256 + threadIdx.x;
+  float contrib = 0.0f;
+  if (n < a.n) {
+    float mx = -INFINITY;
+    for (int t = 0; t < a.tiles; ++t) mx = fmaxf(mx, a.part_m[static_cast<int64_t>(t) * a.ldn + n]);
+    float l = 0.0f;
+    for (int t = 0; t < a.tiles; ++t) {
+      const int64_t o = static_cast<int64_t>(t) * a.ldn + n;
+      l += a.part_l[o] * expf(a.part_m[o] - mx);
+    }
+    const float lse = mx + logf(l);
+    const int y = a.targets[n];
+    const bool ok = y >= 0 && y < a.vocab;
+    if (!ok) *a.flag = 1;
+    const float nll = ok ? lse - a.tgt[n] : NAN;
+    float w = a.token_w != nullptr ? a.token_w[n] : 1.0f;
+    if (a.dynamic_weights) w *= expf(mx - lse);  // detached confidence = max probability
+    const float s = a.exit_weight * w / static_cast<float>(a.n);
+    a.sn[n] = s;
+    for (int t = 0; t < a.tiles; ++t) {
+      const int64_t o = static_cast<int64_t>(t) * a.ldn + n;
+      a.part_m[o] = s * expf(a.part_m[o] - lse);
+    }
+    if (a.row_loss != nullptr) a.row_loss[n] = nll;
+    contrib = w * nll;
+  }
+  red[threadIdx.x] = contrib;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) a.block_sums[blockIdx.x] = red[0];
+}
+
+// In-place seed: each thread owns 8 consecutive tokens of 16 vocab rows.
+template <typename T>
+__global__ __launch_bounds__(256) void seed_kernel(T *P, const float *coef, const float *sn,
+                                                   const int32_t *targets, int n, int ldn, int vocab) {
+  const int c0 = blockIdx.x * 2048 + threadIdx.x * 8;
+  if (c0 >= ldn) return;
+  const int v0 = blockIdx.y * 16;
+  const int tile = v0 / kVocabTile;
+  float cf[8], s[8];
+  int yy[8];
+  bool ok[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int c = c0 + e;
+    ok[e] = c < n;
+    cf[e] = ok[e] ? coef[static_cast<int64_t>(tile) * ldn + c] : 0.0f;
+    s[e] = ok[e] ? sn[c] : 0.0f;
+    yy[e] = ok[e] ? targets[c] : -1;
+  }
+  for (int r = 0; r < 16; ++r) {
+    const int v = v0 + r;
+    if (v >= vocab) break;
+    T *row = P + static_cast<int64_t>(v) * ldn + c0;
+    float p[8], g[8];
+    load_f32<8>(row, p);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) g[e] = ok[e] ? p[e] * cf[e] - (yy[e] == v ? s[e] : 0.0f) : 0.0f;
+    store_f32<8>(row, g);
+  }
+}
+
+__global__ __launch_bounds__(256) void final_loss_kernel(const float *bs, int nb, int n, float *loss,
+                                                         float *total, float w, int first) {
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < nb; i += 256) s += bs[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float L = static_cast<float>(red[0] / static_cast<double>(n));
+    loss[0] = L;
+    if (total != nullptr) total[0] = (first ? 0.0f : total[0]) + w * L;
+  }
+}
+
+__global__ __launch_bounds__(256) void gain_reduce_kernel(const float *pa, int ta, const float *pb, int tb,
+                                                          int h, float *out, int accumulate) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= h) return;
+  float s = 0.0f;
+  for (int t = 0; t < ta; ++t) s += pa[static_cast<int64_t>(t) * h + j];
+  for (int t = 0; t < tb; ++t) s += pb[static_cast<int64_t>(t) * h + j];
+  out[j] = accumulate ? out[j] + s : s;
+}
+
+__global__ void clear_flag_kernel(int *flag) { *flag = 0; }
+
+// -------------------------------------------------------------- launchers
+#define EE_DISPATCH(f32, ...)            \
+  do {                                   \
+    if (f32) {                           \
+      using T = float;                   \
+      __VA_ARGS__;                       \
+    } else {                             \
+      using T = bf16_t;                  \
+      __VA_ARGS__;                       \
+    }                                    \
+  } while (0)
+
+hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps, float *r,
+                          hipStream_t stream) {
+  const dim3 grid(cdiv(n, 4));
+  if (x_f32)
+    hipLaunchKernelGGL(row_rms_kernel<float>, grid, dim3(256), 0, stream, static_cast<const float *>(x), ldx,
+                       n, h, eps, r);
+  else
+    hipLaunchKernelGGL(row_rms_kernel<bf16_t>, grid, dim3(256), 0, stream, static_cast<const bf16_t *>(x),
+                       ldx, n, h, eps, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, const float *r,
+                             const void *gain, int n, int ldn, int h, void *z, void *x_hat, void *x_hat_t,
+                             hipStream_t stream) {
+  const dim3 grid(cdiv(ldn, 64), h / 64);
+  EE_DISPATCH(f32, {
+    if (x_f32)
+      hipLaunchKernelGGL((norm_apply_kernel<float, T>), grid, dim3(256), 0, stream,
+                         static_cast<const float *>(x), ldx, r, static_cast<const T *>(gain), n, ldn, h,
+                         static_cast<T *>(z), static_cast<T *>(x_hat), static_cast<T *>(x_hat_t));
+    else
+      hipLaunchKernelGGL((norm_apply_kernel<bf16_t, T>), grid, dim3(256), 0, stream,
+                         static_cast<const bf16_t *>(x), ldx, r, static_cast<const T *>(gain), n, ldn, h,
+                         static_cast<T *>(z), static_cast<T *>(x_hat), static_cast<T *>(x_hat_t));
+  });
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream) {
+  hipLaunchKernelGGL(ce_reduce_kernel, dim3(cdiv(a.n, 256)), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_seed(bool f32, void *P, const float *coef, const float *sn, const int32_t *targets, int n,
+                       int ldn, int vocab, hipStream_t stream) {
+  const dim3 grid(cdiv(ldn, 2048), cdiv(vocab, 16));
+  EE_DISPATCH(f32, hipLaunchKernelGGL(seed_kernel<T>, grid, dim3(256), 0, stream, static_cast<T *>(P), coef,
+                                      sn, targets, n, ldn, vocab));
+  return hipGetLastError();
+}
+
+hipError_t launch_final_loss(const float *block_sums, int blocks, int n, float *loss, float *total, float w,
+                             int first, hipStream_t stream) {
+  hipLaunchKernelGGL(final_loss_kernel, dim3(1), dim3(256), 0, stream, block_sums, blocks, n, loss, total, w,
+                     first);
+  return hipGetLastError();
+}
+
+hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *part_b, int tiles_b, int h,
+                              float *out, int accumulate, hipStream_t stream) {
+  hipLaunchKernelGGL(gain_reduce_kernel, dim3(cdiv(h, 256)), dim3(256), 0, stream, part_a, tiles_a, part_b,
+                     tiles_b, h, out, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const float *r, const void *gain, int n,
+                           int h, void *dy, hipStream_t stream) {
+  EE_DISPATCH(f32, hipLaunchKernelGGL(norm_bwd_kernel<T>, dim3(cdiv(n, 4)), dim3(256), 0, stream, dz, y, r,
+                                      static_cast<const T *>(gain), n, h, static_cast<T *>(dy)));
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_flag(int *flag, hipStream_t stream) {
+  hipLaunchKernelGGL(clear_flag_kernel, dim3(1), dim3(1), 0, stream, flag);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ GEMMs
+hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, int n, int h, void *P, int ldn,
+                       float *part_m, float *part_l, float *tgt, const int32_t *targets, hipStream_t stream) {
+  EE_DISPATCH(f32, {
+    typename EpiLogits<T>::Params ep{static_cast<T *>(P), ldn, part_m, part_l, tgt, targets};
+    return launch_gemm<T, true, true, EpiLogits<T>>(Operand{w_out, h}, Operand{z, h}, GemmShape{vocab, n, h}, ep,
+                                                    stream);
+  });
+  return hipSuccess;
+}
+
+hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, int m, int h, int ldn,
+                               const void *gain, const void *w, float *dw, float *part, int accumulate,
+                               hipStream_t stream) {
+  EE_DISPATCH(f32, {
+    typename EpiWeightGrad<T>::Params ep{dw, h, static_cast<const T *>(gain), static_cast<const T *>(w), part,
+                                         accumulate};
+    return launch_gemm<T, true, true, EpiWeightGrad<T>>(Operand{g_t, ldn}, Operand{xhat_t, ldn},
+                                                        GemmShape{m, h, ldn}, ep, stream);
+  });
+  return hipSuccess;
+}
+
+hipError_t gemm_weight_grad_mn(bool f32, const void *g, const void *xhat, int m, int h, int n,
+                               const void *gain, const void *w, float *dw, float *part, int accumulate,
+                               hipStream_t stream) {
+  EE_DISPATCH(f32, {
+    typename EpiWeightGrad<T>::Params ep{dw, h, static_cast<const T *>(gain), static_cast<const T *>(w), part,
+                                         accumulate};
+    return launch_gemm<T, false, false, EpiWeightGrad<T>>(Operand{g, m}, Operand{xhat, h}, GemmShape{m, h, n},
+                                                          ep, stream);
+  });
+  return hipSuccess;
+}
+
+hipError_t gemm_gate(bool f32, const void *u, const void *w_gate, int n, int inter, int h, void *hg,
+                     hipStream_t stream) {
+  EE_DISPATCH(f32, {
+    typename EpiStoreT<T>::Params ep{static_cast<T *>(hg), inter};
+    return launch_gemm<T, true, true, EpiStoreT<T>>(Operand{u, h}, Operand{w_gate, h}, GemmShape{n, inter, h},
+                                                    ep, stream);
+  });
+  return hipSuccess;
+}
+
+hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int inter, int h, const void *hg,
+                          void *hu, void *act, hipStream_t stream) {
+  EE_DISPATCH(f32, {
+    typename EpiSwiGLU<T>::Params ep{static_cast<const T *>(hg), static_cast<T *>(hu), static_cast<T *>(act),
+                                     inter};
+    return launch_gemm<T, true, true, EpiSwiGLU<T>>(Operand{u, h}, Operand{w_up, h}, GemmShape{n, inter, h}, ep,
+                                                    stream);
+  });
+  return hipSuccess;
+}
+
+hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, const void *x, int n, int h,
+                              int inter, float *y, hipStream_t stream) {
+  EE_DISPATCH(f32, {
+    typename EpiStoreF32<T>::Params ep{y, h, static_cast<const T *>(x), h, n, 0};
+    return launch_gemm<T, true, true, EpiStoreF32<T>>(Operand{act, inter}, Operand{w_down, inter},
+                                                      GemmShape{n, h, inter}, ep, stream);
+  });
+  return hipSuccess;
+}
+
+hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab, float *dz,
+                   hipStream_t stream) {
+  EE_DISPATCH(f32, {
+    typename EpiStoreF32<T>::Params ep{dz, h, nullptr, 0, n, 0};
+    return launch_gemm<T, false, false, EpiStoreF32<T>>(Operand{g_t, ldn}, Operand{w_out, h},
+                                                        GemmShape{ldn, h, vocab}, ep, stream);
+  });
+  return hipSuccess;
+}
+
+hipError_t gemm_da_swiglu(bool f32, const void *dy, const void *w_down, int n, int inter, int h, const void *hg,
+                          const void *hu, void *dhg, void *dhu, hipStream_t stream) {
+  EE_DISPATCH(f32, {
+    typename EpiSwiGLUBwd<T>::Params ep{static_cast<const T *>(hg), static_cast<const T *>(hu),
+                                        static_cast<T *>(dhg), static_cast<T *>(dhu), inter};
+    return launch_gemm<T, true, false, EpiSwiGLUBwd<T>>(Operand{dy, h}, Operand{w_down, inter},
+                                                        GemmShape{n, inter, h}, ep, stream);
+  });
+  return hipSuccess;
+}
+
+hipError_t gemm_dw_down(bool f32, const void *dy, const void *act, int n, int h, int inter, float *dwd,
+                        int accumulate, hipStream_t stream) {
+  EE_DISPATCH(f32, {
+    typename EpiStoreF32<T>::Params ep{dwd, inter, nullptr, 0, h, accumulate};
+    return launch_gemm<T, false, false, EpiStoreF32<T>>(Operand{dy, h}, Operand{act, inter},
+                                                        GemmShape{h, inter, n}, ep, stream);
+  });
+  return hipSuccess;
+}
+
+}  // namespace ee

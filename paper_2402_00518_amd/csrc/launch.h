@@ -1,0 +1,97 @@
+// Host-callable launchers of the exit-head kernels (defined in kernels.hip).
+// Every launcher enqueues on `stream` and returns the launch status; shapes
+// have been validated by the caller.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ee {
+
+// Tile sizes the workspace layout depends on.
+constexpr int kVocabTile = 128;   // rows of a GEMM output tile
+constexpr int kTokenPad = 64;     // padding of the token dimension
+
+// Row-wise RMSNorm scale r[n] = (mean_j x[n][j]^2 + eps)^(-1/2).
+hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps,
+                          float *r, hipStream_t stream);
+
+// Apply a row scale and a gain: x_hat = x * r[n] (r == NULL: x_hat = x), z = x_hat * gain.
+// Writes any of z [n][h], x_hat [n][h] (row-major) and x_hat^T [h][ldn]
+// (token-contiguous, columns n..ldn-1 zero).  Output element type = `f32`.
+hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, const float *r,
+                             const void *gain, int n, int ldn, int h, void *z, void *x_hat,
+                             void *x_hat_t, hipStream_t stream);
+
+// Combine the per-tile softmax partials of each token into LSE, the row NLL,
+// the loss-weight s_n and the per-tile seed coefficients (written over
+// part_m).  Also flags targets outside [0, V).
+struct CeReduceArgs {
+  float *part_m;          // in: tile max; out: s_n * exp(m_tile - LSE)
+  const float *part_l;
+  const float *tgt;
+  const int32_t *targets;
+  const float *token_w;   // or NULL
+  float *sn;              // [ldn] s_n
+  float *row_loss;        // [n] or NULL
+  float *block_sums;      // [cdiv(n, 256)]
+  int *flag;
+  int n, ldn, vocab, tiles;
+  float exit_weight;
+  int dynamic_weights;
+};
+hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream);
+
+// In place: G[v][n] = P[v][n] * coef[v / 128][n] - (v == y_n) * s_n  (0 for n >= N).
+hipError_t launch_seed(bool f32, void *P, const float *coef, const float *sn, const int32_t *targets,
+                       int n, int ldn, int vocab, hipStream_t stream);
+
+// loss[0] = sum(block_sums) / n;  total[0] = (first ? 0 : total[0]) + w * loss[0].
+hipError_t launch_final_loss(const float *block_sums, int blocks, int n, float *loss, float *total,
+                             float w, int first, hipStream_t stream);
+
+// out[j] (=|+=) sum_t part_a[t][j] (+ sum_t part_b[t][j]).
+hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *part_b, int tiles_b,
+                              int h, float *out, int accumulate, hipStream_t stream);
+
+// RMSNorm backward through the exit norm of an MLP exit:
+//   dz_hat = dZ * gain,  z_hat = y * r,  dY = r (dz_hat - z_hat mean_j(dz_hat z_hat)).
+hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const float *r, const void *gain,
+                           int n, int h, void *dy, hipStream_t stream);
+
+hipError_t launch_clear_flag(int *flag, hipStream_t stream);
+
+// ------------------------------------------------------------------ GEMMs
+// Logits^T = W_out Z^T with the softmax-partials epilogue.
+hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, int n, int h, void *P,
+                       int ldn, float *part_m, float *part_l, float *tgt, const int32_t *targets,
+                       hipStream_t stream);
+// dW[M][h] = (G^T X_hat) * gain with gain-gradient partials (K = tokens, both operands
+// token-contiguous with leading dimension ldn).
+hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, int m, int h, int ldn,
+                               const void *gain, const void *w, float *dw, float *part, int accumulate,
+                               hipStream_t stream);
+// Same, operands stored row-major over tokens: g [n][m], xhat [n][h].
+hipError_t gemm_weight_grad_mn(bool f32, const void *g, const void *xhat, int m, int h, int n,
+                               const void *gain, const void *w, float *dw, float *part, int accumulate,
+                               hipStream_t stream);
+// H_g[n][I] = U W_gate^T.
+hipError_t gemm_gate(bool f32, const void *u, const void *w_gate, int n, int inter, int h, void *hg,
+                     hipStream_t stream);
+// H_u = U W_up^T, A = silu(H_g) H_u.
+hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int inter, int h,
+                          const void *hg, void *hu, void *act, hipStream_t stream);
+// Y[n][h] = X + A W_down^T  (fp32 out).
+hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, const void *x, int n,
+                              int h, int inter, float *y, hipStream_t stream);
+// dZ[n][h] = G W_out with G stored transposed [V][ldn]  (fp32 out).
+hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab,
+                   float *dz, hipStream_t stream);
+// dA = dY W_down with the SwiGLU backward epilogue.
+hipError_t gemm_da_swiglu(bool f32, const void *dy, const void *w_down, int n, int inter, int h,
+                          const void *hg, const void *hu, void *dhg, void *dhu, hipStream_t stream);
+// dW_down[h][I] (=|+=) dY^T A.
+hipError_t gemm_dw_down(bool f32, const void *dy, const void *act, int n, int h, int inter, float *dwd,
+                        int accumulate, hipStream_t stream);
+
+}  // namespace ee

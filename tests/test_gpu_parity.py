@@ -1,0 +1,274 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Tolerances (bf16 inputs, fp32 accumulation): loss relative error 1e-3;
+every gradient tensor relative L2 error 2e-2.  The fp32 path is held to
+1e-5 / 1e-4.  Small shapes are compared in full and span several tiles
+with ragged tails; the full-size workloads compare the loss, every row's
+NLL, the gains' gradients in full and sampled rows of the weight gradients.
+"""
+
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+LOSS_RTOL = 1e-3
+GRAD_RTOL = 2e-2
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2402_00518_amd import binding
+    binding.lib()          # fail loudly if the library is missing
+    yield
+
+
+def rel_l2(got, ref):
+    ref = np.asarray(ref, dtype=np.float64)
+    got = np.asarray(got, dtype=np.float64)
+    den = np.linalg.norm(ref)
+    if den < 1e-12:
+        return float(np.max(np.abs(got))) if got.size else 0.0
+    return float(np.linalg.norm(got - ref) / den)
+
+
+def host(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def run(batch, flags=0, accumulate=0, steps=1):
+    from paper_2402_00518_amd.session import Session
+    s = Session.from_batch(batch)
+    for _ in range(steps):
+        s.step(flags=flags, accumulate=accumulate)
+    torch.cuda.synchronize()
+    s.check_device_error()
+    return s
+
+
+def oracle_full(batch, dynamic=False):
+    w = batch.workload
+    exits = O.exits_from_batch(batch)
+    xs = [W.decode(x) for x in batch.hidden]
+    return O.multi_exit_step(exits, xs, batch.targets, list(w.exit_weights),
+                             batch.token_weights, dynamic)
+
+
+def compare_full(sess, batch, loss_rtol=LOSS_RTOL, grad_rtol=GRAD_RTOL, dynamic=False):
+    total, per = oracle_full(batch, dynamic)
+    got_total = float(sess.loss_total.item())
+    assert abs(got_total - total) <= loss_rtol * abs(total), (got_total, total)
+    for e, r in enumerate(per):
+        got = float(sess.loss_per_exit[e].item())
+        assert abs(got - r.loss) <= loss_rtol * abs(r.loss), (e, got, r.loss)
+        for name, ref in r.grads.items():
+            err = rel_l2(host(sess.grads[e]["d_" + name]), ref)
+            say(f"  exit {e} d_{name}: rel_l2 {err:.2e}")
+            assert err <= grad_rtol, (e, name, err)
+    return total, per
+
+
+def small(kind, n, h, v, inter=0, dtype="bf16", weights=(1.0,), seed=0, random_gamma=True,
+          token_weights=False, name="small"):
+    w = W.custom(kind, n, h, v, inter, dtype, weights, row_scale=True, zipf=True, name=name)
+    return W.make_batch(w, seed, random_gamma=random_gamma, token_weights=token_weights)
+
+
+# ------------------------------------------------------------------ small cases
+def test_tiny_f32_workload_full_parity():
+    """512 tokens, h 256, V 1024, fp32, single Norm exit (gain 1)."""
+    say("case: tiny_norm_f32 seed 0")
+    b = W.make_batch(W.WORKLOADS["tiny_norm_f32"], 0)
+    s = run(b)
+    compare_full(s, b, loss_rtol=1e-5, grad_rtol=1e-4)
+
+
+SMALL_CASES = [
+    ("norm_ragged", W.EXIT_NORM, 300, 192, 1000, 0, "bf16", False),
+    ("norm_ragged_tokw", W.EXIT_NORM, 300, 192, 1000, 0, "bf16", True),
+    ("embedding_ragged", W.EXIT_EMBEDDING, 200, 128, 777, 0, "bf16", False),
+    ("mlp_ragged", W.EXIT_MLP, 260, 192, 900, 320, "bf16", False),
+    ("mlp_ragged_tokw", W.EXIT_MLP, 130, 128, 513, 192, "bf16", True),
+    ("norm_f32_ragged", W.EXIT_NORM, 70, 64, 333, 0, "f32", False),
+    ("mlp_f32_ragged", W.EXIT_MLP, 150, 128, 300, 192, "f32", True),
+    ("embedding_f32", W.EXIT_EMBEDDING, 129, 64, 129, 0, "f32", False),
+    ("norm_one_token", W.EXIT_NORM, 1, 64, 50, 0, "bf16", False),
+    ("norm_vocab_one", W.EXIT_NORM, 37, 64, 1, 0, "bf16", False),
+    ("norm_multi_tile", W.EXIT_NORM, 1000, 512, 2000, 0, "bf16", False),
+]
+
+
+@pytest.mark.parametrize("name,kind,n,h,v,inter,dtype,tokw", SMALL_CASES, ids=[c[0] for c in SMALL_CASES])
+def test_small_full_parity(name, kind, n, h, v, inter, dtype, tokw):
+    say(f"case: {name} N={n} h={h} V={v} I={inter} {dtype}")
+    b = small(kind, n, h, v, inter, dtype, seed=3, token_weights=tokw, name=name)
+    s = run(b)
+    tight = dtype == "f32"
+    compare_full(s, b, loss_rtol=1e-5 if tight else LOSS_RTOL, grad_rtol=1e-4 if tight else GRAD_RTOL)
+
+
+def test_row_losses_match():
+    say("case: row losses norm_ragged")
+    b = small(W.EXIT_NORM, 300, 192, 1000, seed=5, name="rows")
+    from paper_2402_00518_amd.session import Session
+    s = Session.from_batch(b)
+    s.forward(0)
+    torch.cuda.synchronize()
+    r = O.exit_step(O.exits_from_batch(b)[0], W.decode(b.hidden[0]), b.targets)
+    got = host(s.row_loss)
+    assert np.max(np.abs(got - r.row_loss) / np.maximum(1.0, np.abs(r.row_loss))) < 5e-3
+    assert abs(float(s.loss_per_exit[0].item()) - r.loss) <= LOSS_RTOL * r.loss
+
+
+def test_two_exits_mixed_kinds_weighted():
+    say("case: two exits norm + mlp, weights 0.25 0.5")
+    from paper_2402_00518_amd.session import Session
+    bn = small(W.EXIT_NORM, 257, 128, 700, weights=(0.25,), seed=11, name="a")
+    bm = small(W.EXIT_MLP, 257, 128, 700, 192, weights=(0.5,), seed=12, name="b")
+    bm.targets = bn.targets
+    exits = []
+    for p in (bn.exits[0], bm.exits[0]):
+        d = {"w_out": p.w_out, "gamma": p.gamma, "gamma_mlp": p.gamma_mlp, "w_gate": p.w_gate,
+             "w_up": p.w_up, "w_down": p.w_down}
+        exits.append({k: v for k, v in d.items() if v is not None})
+    s = Session(W.EXIT_NORM, 1, 128, 700, 192, 1e-5, exits, [bn.hidden[0], bm.hidden[0]], bn.targets,
+                None, (0.25, 0.5), kinds=[W.EXIT_NORM, W.EXIT_MLP])
+    s.step()
+    torch.cuda.synchronize()
+    oe = O.exits_from_batch(bn) + O.exits_from_batch(bm)
+    total, per = O.multi_exit_step(oe, [W.decode(bn.hidden[0]), W.decode(bm.hidden[0])], bn.targets,
+                                   [0.25, 0.5])
+    assert abs(s.loss_total.item() - total) <= LOSS_RTOL * total
+    for e in range(2):
+        for name, ref in per[e].grads.items():
+            assert rel_l2(host(s.grads[e]["d_" + name]), ref) <= GRAD_RTOL, (e, name)
+
+
+def test_dynamic_token_weights():
+    say("case: dynamic token-wise weights, norm")
+    from paper_2402_00518_amd.binding import EE_FLAG_DYNAMIC_TOKEN_WEIGHTS
+    b = small(W.EXIT_NORM, 300, 192, 500, seed=21, name="dyn")
+    # larger output weights so that confidences vary between tokens
+    b.exits[0].w_out = W.f32_to_bf16_bits(W.decode(b.exits[0].w_out).astype(np.float32) * 10)
+    s = run(b, flags=EE_FLAG_DYNAMIC_TOKEN_WEIGHTS)
+    compare_full(s, b, dynamic=True)
+
+
+# ------------------------------------------------------------ properties
+def test_zero_output_matrix_gives_ln_v():
+    say("case: W_out = 0")
+    b = small(W.EXIT_NORM, 200, 128, 1000, seed=31, name="zero")
+    b.exits[0].w_out[:] = 0
+    s = run(b)
+    assert abs(s.loss_total.item() - math.log(1000)) < 1e-5 * math.log(1000)
+    assert np.all(host(s.grads[0]["d_gamma"]) == 0.0)
+    # sum over the vocabulary of the output-matrix gradient vanishes
+    col = host(s.grads[0]["d_w_out"]).sum(axis=0)
+    assert np.max(np.abs(col)) < 1e-6
+
+
+def test_deterministic_and_accumulate():
+    say("case: determinism + accumulate, mlp")
+    b = small(W.EXIT_MLP, 200, 128, 600, 192, seed=41, name="det")
+    s1, s2 = run(b), run(b)
+    for k in s1.grads[0]:
+        assert torch.equal(s1.grads[0][k], s2.grads[0][k]), k
+    assert torch.equal(s1.loss_total, s2.loss_total)
+    s3 = run(b, accumulate=1, steps=2)
+    for k in s1.grads[0]:
+        assert torch.allclose(s3.grads[0][k], 2 * s1.grads[0][k], rtol=1e-6, atol=0), k
+
+
+def test_aliased_weights_give_identical_gradients():
+    say("case: two exits aliasing one parameter set")
+    from paper_2402_00518_amd import binding as B
+    from paper_2402_00518_amd.session import Session
+    b = small(W.EXIT_NORM, 150, 128, 400, seed=51, name="alias")
+    p = b.exits[0]
+    ex = {"w_out": p.w_out, "gamma": p.gamma}
+    s = Session(W.EXIT_NORM, 1, 128, 400, 0, 1e-5, [ex, ex], [b.hidden[0], b.hidden[0]], b.targets,
+                None, (1.0, 1.0))
+    # point exit 1 at exit 0's parameter and hidden buffers (copy init shares weights)
+    s.c_exits[1] = B.make_exit(W.EXIT_NORM, 1, 128, 400, 0, 1e-5, **s.params[0])
+    s.x[1] = s.x[0]
+    s.step()
+    torch.cuda.synchronize()
+    for k in s.grads[0]:
+        assert torch.equal(s.grads[0][k], s.grads[1][k]), k
+
+
+def test_out_of_range_target_is_reported():
+    say("case: target outside the vocabulary")
+    from paper_2402_00518_amd import binding as B
+    from paper_2402_00518_amd.session import Session
+    b = small(W.EXIT_NORM, 100, 64, 300, seed=61, name="bad")
+    b.targets[7] = 300
+    s = Session.from_batch(b)
+    s.step()
+    with pytest.raises(B.EEError) as ei:
+        s.check_device_error()
+    assert ei.value.status == B.EE_ERR_TARGET
+    assert math.isnan(s.loss_total.item())
+    s.check_device_error()            # the record was cleared
+    b.targets[7] = 0
+    s2 = Session.from_batch(b)
+    s2.step()
+    s2.check_device_error()
+
+
+# ----------------------------------------------------- full-size workloads
+def sampled_compare(name, seed=0, random_gamma=False):
+    w = W.WORKLOADS[name]
+    say(f"case: {name} full size seed {seed} random_gamma {random_gamma}")
+    b = W.make_batch(w, seed, random_gamma=random_gamma)
+    s = run(b)
+    exits = O.exits_from_batch(b)
+    counts = np.bincount(b.targets, minlength=w.vocab)
+    v_rows = np.unique(np.concatenate([W.row_sample(w.vocab, 24, seed), np.argsort(counts)[-4:]]))
+    i_rows = W.row_sample(w.intermediate, 12, seed) if w.kind == W.EXIT_MLP else None
+    total = 0.0
+    for e, (ex, wt) in enumerate(zip(exits, w.exit_weights)):
+        ref = O.exit_step_sampled(ex, W.decode(b.hidden[e]), b.targets, wt, v_rows, i_rows)
+        L = float(ref["loss"])
+        total += wt * L
+        got = float(s.loss_per_exit[e].item())
+        say(f"  exit {e} loss gpu {got:.6f} oracle {L:.6f}")
+        assert abs(got - L) <= LOSS_RTOL * abs(L)
+        g = s.grads[e]
+        checks = [("d_w_out rows", host(g["d_w_out"][torch.as_tensor(v_rows).cuda()]), ref["w_out_rows"])]
+        if ex.kind != W.EXIT_EMBEDDING:
+            checks.append(("d_gamma", host(g["d_gamma"]), ref["gamma"]))
+        if ex.kind == W.EXIT_MLP:
+            ir = torch.as_tensor(i_rows).cuda()
+            checks += [("d_gamma_mlp", host(g["d_gamma_mlp"]), ref["gamma_mlp"]),
+                       ("d_w_gate rows", host(g["d_w_gate"][ir]), ref["w_gate_rows"]),
+                       ("d_w_up rows", host(g["d_w_up"][ir]), ref["w_up_rows"]),
+                       ("d_w_down cols", host(g["d_w_down"][:, ir]), ref["w_down_cols"])]
+        for label, got_g, ref_g in checks:
+            err = rel_l2(got_g, ref_g)
+            say(f"  exit {e} {label}: rel_l2 {err:.2e}")
+            assert err <= GRAD_RTOL, (label, err)
+    assert abs(s.loss_total.item() - total) <= LOSS_RTOL * abs(total)
+
+
+@pytest.mark.parametrize("name", ["llama7b_norm", "llama7b_norm_2exits", "llama13b_mlp", "llama70b_norm"])
+def test_full_size_sampled_parity(name):
+    sampled_compare(name)
+
+
+def test_full_size_random_gamma():
+    sampled_compare("llama7b_norm", seed=1, random_gamma=True)
