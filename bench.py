@@ -94,7 +94,7 @@ def cpu_baseline(batch, sample_tokens):
     except Exception:
         threads = 1
     w = batch.workload
-    n = min(sample_tokens, w.n_tokens)
+    n = w.n_tokens if sample_tokens <= 0 else min(sample_tokens, w.n_tokens)
     exits = O.exits_from_batch(batch)
     xs = [W.decode(x[:n]) for x in batch.hidden]
     y = batch.targets[:n]
@@ -114,7 +114,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama7b_norm")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-sample-tokens", type=int, default=512)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=0,
+                    help="tokens of the batch the oracle runs on (0: all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-pass", action="store_true")
     args = ap.parse_args()
@@ -203,7 +204,7 @@ def main():
         log(f"dominant kernel {dom}: {kernels[dom]['avg_ms']:.4f} ms")
 
     if not args.no_cpu_baseline:
-        log(f"cpu baseline: oracle on {args.cpu_sample_tokens} tokens ...")
+        log("cpu baseline: oracle on the batch ...")
         out["cpu_baseline"] = cpu_baseline(batch, args.cpu_sample_tokens)
         log(f"cpu baseline {out['cpu_baseline']['value']:.1f} tokens/s")
 

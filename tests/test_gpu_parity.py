@@ -176,9 +176,13 @@ def test_zero_output_matrix_gives_ln_v():
     s = run(b)
     assert abs(s.loss_total.item() - math.log(1000)) < 1e-5 * math.log(1000)
     assert np.all(host(s.grads[0]["d_gamma"]) == 0.0)
-    # sum over the vocabulary of the output-matrix gradient vanishes
+    # Each seed row sums to zero up to bf16 rounding: sum_v |G[n, v]| <= 2 s_n and
+    # bf16 keeps 8 significant bits, so |sum_v G[n, v]| <= 2^-7 s_n; the column
+    # sums of dW_out = G^T Z are then bounded by 2^-7 sum_n s_n |Z[n, j]|.
     col = host(s.grads[0]["d_w_out"]).sum(axis=0)
-    assert np.max(np.abs(col)) < 1e-6
+    z = O.exit_forward(O.exits_from_batch(b)[0], W.decode(b.hidden[0]))["z"]
+    bound = 2.0 ** -7 * np.sum(np.abs(z), axis=0) / 200 + 1e-6
+    assert np.all(np.abs(col) <= bound)
 
 
 def test_deterministic_and_accumulate():
