@@ -41,7 +41,8 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 // by every exit: the device error flag and a scratch loss slot.
 struct Layout {
   int64_t ldn = 0, vtiles = 0, itiles = 0;
-  size_t z = 0, zht = 0, r = 0, P = 0, pm = 0, pl = 0, tgt = 0, sn = 0, bsum = 0, dgp = 0;
+  int vtile = 0, itile = 0;
+  size_t z = 0, zht = 0, r = 0, P = 0, pm = 0, pl = 0, tgt = 0, lse = 0, sn = 0, bsum = 0, dgp = 0;
   size_t u = 0, uhat = 0, rx = 0, hg = 0, hu = 0, act = 0, y = 0, dz = 0, dy = 0, dhg = 0, dhu = 0,
          dgpg = 0, dgpu = 0;
   size_t total = 0;
@@ -56,8 +57,11 @@ Layout layout(const ee_exit &e, int64_t n) {
   const size_t h = static_cast<size_t>(e.hidden), V = static_cast<size_t>(e.vocab);
   const size_t I = static_cast<size_t>(e.intermediate), N = static_cast<size_t>(n);
   L.ldn = cdiv64(n, ee::kTokenPad) * ee::kTokenPad;
-  L.vtiles = cdiv64(e.vocab, ee::kVocabTile);
-  L.itiles = cdiv64(e.intermediate, ee::kVocabTile);
+  const bool f32 = e.dtype == EE_F32;
+  L.vtile = ee::gemm_tile_rows(f32, true, true);     // logits and dW_out GEMMs
+  L.itile = ee::gemm_tile_rows(f32, false, false);   // dW_gate / dW_up GEMMs
+  L.vtiles = cdiv64(e.vocab, L.vtile);
+  L.itiles = cdiv64(e.intermediate, L.itile);
   const size_t ldn = static_cast<size_t>(L.ldn);
   size_t cur = kHeader;
   auto take = [&](size_t bytes) {
@@ -73,8 +77,9 @@ Layout layout(const ee_exit &e, int64_t n) {
   L.pm = take(static_cast<size_t>(L.vtiles) * ldn * 4);
   L.pl = take(static_cast<size_t>(L.vtiles) * ldn * 4);
   L.tgt = take(ldn * 4);
+  L.lse = take(ldn * 4);
   L.sn = take(ldn * 4);
-  L.bsum = take(static_cast<size_t>(cdiv64(n, 256)) * 4);
+  L.bsum = take(static_cast<size_t>(cdiv64(n, 32)) * 4);
   if (normed) L.dgp = take(static_cast<size_t>(L.vtiles) * h * 4);
   if (e.kind == EE_EXIT_MLP) {
     L.u = take(N * h * es);
@@ -299,6 +304,7 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   a.tgt = atf(ws, L.tgt);
   a.targets = targets;
   a.token_w = token_w;
+  a.lse = atf(ws, L.lse);
   a.sn = atf(ws, L.sn);
   a.row_loss = row_loss;
   a.block_sums = atf(ws, L.bsum);
@@ -310,8 +316,8 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   a.exit_weight = w_e;
   a.dynamic_weights = (flags & EE_FLAG_DYNAMIC_TOKEN_WEIGHTS) ? 1 : 0;
   EE_LAUNCH("cross-entropy reduce", s, ee::launch_ce_reduce(a, s));
-  EE_LAUNCH("logit seed", s, ee::launch_seed(f32, at(ws, L.P), atf(ws, L.pm), atf(ws, L.sn), targets, n, ldn, V, s));
-  EE_LAUNCH("loss reduce", s, ee::launch_final_loss(atf(ws, L.bsum), static_cast<int>(cdiv64(n, 256)), n, loss, total, w_e, first, s));
+  EE_LAUNCH("logit seed", s, ee::launch_seed(f32, at(ws, L.P), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), targets, n, ldn, V, L.vtile, s));
+  EE_LAUNCH("loss reduce", s, ee::launch_final_loss(atf(ws, L.bsum), static_cast<int>(cdiv64(n, 32)), n, loss, total, w_e, first, s));
   return EE_OK;
 }
 

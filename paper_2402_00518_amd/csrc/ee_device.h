@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace ee {
 
 typedef uint16_t bf16_t;  // bfloat16 storage bits
@@ -15,6 +18,21 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
+
+// Lambdas that touch register arrays must be inlined: an out-of-line call
+// would take the arrays' address and move them to scratch memory.
+#define EE_ALWAYS_INLINE __attribute__((always_inline))
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I = 0..N-1, so
+// that register arrays indexed by I are never addressed dynamically.
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_impl(static_cast<F &&>(f), std::make_integer_sequence<int, N>{});
+}
 
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);

@@ -1,11 +1,52 @@
-// Fused epilogues of the exit-head GEMMs.  Each receives the wave's 2 x 2
-// block of 32 x 32 fp32 accumulators and the tile context (see gemm.h for
-// the accumulator-to-(row, col) map).
+// Fused epilogues of the exit-head GEMMs.  Each receives the wave's MB x NB
+// blocks of 32 x 32 fp32 accumulators and the tile context (see gemm.h for
+// the accumulator-to-(row, col) map).  Accumulators are only ever indexed
+// with compile-time indices (for_each_acc), so they stay in registers.
 #pragma once
 
 #include "gemm.h"
 
 namespace ee {
+
+// f(row, col, j, value) for every accumulator element of the lane; j is the
+// lane's column slot (0..NB-1).
+template <class Cfg, class F>
+__device__ __forceinline__ void for_each_acc(f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t, F &&f) {
+  static_for<Cfg::MB>([&](auto i) EE_ALWAYS_INLINE {
+    static_for<16>([&](auto v) EE_ALWAYS_INLINE {
+      const int row = t.row(i, v);
+      static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE { f(row, t.col(j), static_cast<int>(j), acc[i][j][decltype(v)::value]); });
+    });
+  });
+}
+
+// Same, with operands the epilogue reads from memory: for each 32-row block
+// first every load(row_c, col_c) of the block is issued (rows and columns
+// clamped into [0, rows) x [0, cols), so no load is predicated), then
+// f(row, col, j, value, loaded) runs for the block.  Loads therefore never
+// wait behind the stores of the same block.
+template <class Cfg, class L, class F>
+__device__ __forceinline__ void for_each_acc_loaded(f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t, int rows,
+                                                    int cols, L &&load, F &&f) {
+  using V = decltype(load(0, 0));
+  static_for<Cfg::MB>([&](auto i) EE_ALWAYS_INLINE {
+    V pre[16][Cfg::NB];
+    static_for<16>([&](auto v) EE_ALWAYS_INLINE {
+      const int row = min(t.row(i, v), rows - 1);
+      static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE { pre[v][j] = load(row, min(t.col(j), cols - 1)); });
+    });
+    static_for<16>([&](auto v) EE_ALWAYS_INLINE {
+      const int row = t.row(i, v);
+      static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE {
+        f(row, t.col(j), static_cast<int>(j), acc[i][j][decltype(v)::value], pre[v][j]);
+      });
+    });
+  });
+}
+
+struct F2 {
+  float a, b;
+};
 
 // Logits, transposed: C[v][n] = S[n][v] = Z[n] . W_out[v]  (rows = vocab ids,
 // columns = tokens).  Per (vocab tile, token) it keeps the online-softmax
@@ -22,56 +63,40 @@ struct EpiLogits {
     float *tgt;         // [ldp] target logit
     const int32_t *targets;
   };
-  __device__ static void apply(const Params &p, f32x16_t (&acc)[2][2], const TileCtx &t) {
-    int y[2];
-    float mx[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    constexpr int NB = Cfg::NB;
+    int y[NB];
+    float mx[NB], sm[NB];
+    static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
       const int col = t.col(j);
       y[j] = col < t.N ? p.targets[col] : -1;
       mx[j] = -INFINITY;
-    }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = t.row(i, v);
-        if (row < t.M) {
-#pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            const float a = acc[i][j][v];
-            mx[j] = fmaxf(mx[j], a);
-            if (row == y[j]) p.tgt[t.col(j)] = a;
-          }
-        }
+      sm[j] = 0.0f;
+    });
+    for_each_acc<Cfg>(acc, t, [&](int row, int col, int j, float a) EE_ALWAYS_INLINE {
+      if (row < t.M) {
+        mx[j] = fmaxf(mx[j], a);
+        if (row == y[j]) p.tgt[col] = a;
       }
-    tile_col_reduce<true>(t, mx);
-    float sm[2] = {0.0f, 0.0f};
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = t.row(i, v);
-        if (row < t.M) {
-#pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            const int col = t.col(j);
-            const float e = fast_exp(acc[i][j][v] - mx[j]);
-            sm[j] += e;
-            if (col < t.N) p.P[static_cast<int64_t>(row) * p.ldp + col] = from_f32<T>(e);
-          }
-        }
+    });
+    tile_col_reduce<true, Cfg>(t, mx);
+    for_each_acc<Cfg>(acc, t, [&](int row, int col, int j, float a) EE_ALWAYS_INLINE {
+      if (row < t.M) {
+        const float e = fast_exp(a - mx[j]);
+        sm[j] += e;
+        if (col < t.N) p.P[static_cast<int64_t>(row) * p.ldp + col] = from_f32<T>(e);
       }
-    tile_col_reduce<false>(t, sm);
+    });
+    tile_col_reduce<false, Cfg>(t, sm);
     if (t.wave_m == 0 && t.lane < 32) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
         const int col = t.col(j);
         if (col < t.N) {
           p.part_m[static_cast<int64_t>(t.tile_m) * p.ldp + col] = mx[j];
           p.part_l[static_cast<int64_t>(t.tile_m) * p.ldp + col] = sm[j];
         }
-      }
+      });
     }
   }
 };
@@ -93,38 +118,35 @@ struct EpiWeightGrad {
     float *part;        // [tiles over M][ldw]
     int accumulate;
   };
-  __device__ static void apply(const Params &p, f32x16_t (&acc)[2][2], const TileCtx &t) {
-    float g[2], dg[2] = {0.0f, 0.0f};
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    constexpr int NB = Cfg::NB;
+    float g[NB], dg[NB];
+    static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
       const int col = t.col(j);
       g[j] = (p.gain != nullptr && col < t.N) ? to_f32(p.gain[col]) : 1.0f;
-    }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = t.row(i, v);
-        if (row >= t.M) continue;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int col = t.col(j);
-          if (col >= t.N) continue;
+      dg[j] = 0.0f;
+    });
+    const bool with_w = p.W != nullptr;
+    for_each_acc_loaded<Cfg>(
+        acc, t, t.M, t.N,
+        [&](int row, int col) EE_ALWAYS_INLINE {
           const int64_t o = static_cast<int64_t>(row) * p.ldw + col;
-          const float c = acc[i][j][v];
-          const float d = c * g[j];
-          p.dW[o] = p.accumulate ? p.dW[o] + d : d;
-          if (p.W != nullptr) dg[j] += to_f32(p.W[o]) * c;
-        }
-      }
-    if (p.W != nullptr) {
-      tile_col_reduce<false>(t, dg);
+          return F2{with_w ? to_f32(p.W[o]) : 0.0f, p.accumulate ? p.dW[o] : 0.0f};
+        },
+        [&](int row, int col, int j, float c, F2 in) EE_ALWAYS_INLINE {
+          if (row < t.M && col < t.N) {
+            p.dW[static_cast<int64_t>(row) * p.ldw + col] = in.b + c * g[j];
+            dg[j] += in.a * c;
+          }
+        });
+    if (with_w) {
+      tile_col_reduce<false, Cfg>(t, dg);
       if (t.wave_m == 0 && t.lane < 32) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
           const int col = t.col(j);
           if (col < t.N) p.part[static_cast<int64_t>(t.tile_m) * p.ldw + col] = dg[j];
-        }
+        });
       }
     }
   }
@@ -142,23 +164,19 @@ struct EpiStoreF32 {
     int rows;
     int accumulate;
   };
-  __device__ static void apply(const Params &p, f32x16_t (&acc)[2][2], const TileCtx &t) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = t.row(i, v);
-        if (row >= p.rows) continue;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int col = t.col(j);
-          if (col >= t.N) continue;
-          float c = acc[i][j][v];
-          if (p.residual != nullptr) c += to_f32(p.residual[static_cast<int64_t>(row) * p.ldr + col]);
-          const int64_t o = static_cast<int64_t>(row) * p.ldc + col;
-          p.C[o] = p.accumulate ? p.C[o] + c : c;
-        }
-      }
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    for_each_acc_loaded<Cfg>(
+        acc, t, p.rows, t.N,
+        [&](int row, int col) EE_ALWAYS_INLINE {
+          float r = 0.0f;
+          if (p.residual != nullptr) r += to_f32(p.residual[static_cast<int64_t>(row) * p.ldr + col]);
+          if (p.accumulate) r += p.C[static_cast<int64_t>(row) * p.ldc + col];
+          return r;
+        },
+        [&](int row, int col, int, float a, float in) EE_ALWAYS_INLINE {
+          if (row < p.rows && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = a + in;
+        });
   }
 };
 
@@ -169,19 +187,11 @@ struct EpiStoreT {
     T *C;
     int64_t ldc;
   };
-  __device__ static void apply(const Params &p, f32x16_t (&acc)[2][2], const TileCtx &t) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = t.row(i, v);
-        if (row >= t.M) continue;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int col = t.col(j);
-          if (col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = from_f32<T>(acc[i][j][v]);
-        }
-      }
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    for_each_acc<Cfg>(acc, t, [&](int row, int col, int, float a) EE_ALWAYS_INLINE {
+      if (row < t.M && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = from_f32<T>(a);
+    });
   }
 };
 
@@ -194,24 +204,18 @@ struct EpiSwiGLU {
     T *A;
     int64_t ld;
   };
-  __device__ static void apply(const Params &p, f32x16_t (&acc)[2][2], const TileCtx &t) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = t.row(i, v);
-        if (row >= t.M) continue;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int col = t.col(j);
-          if (col >= t.N) continue;
-          const int64_t o = static_cast<int64_t>(row) * p.ld + col;
-          const float hu = acc[i][j][v];
-          const float hg = to_f32(p.Hg[o]);
-          p.Hu[o] = from_f32<T>(hu);
-          p.A[o] = from_f32<T>(silu_f(hg) * hu);
-        }
-      }
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    for_each_acc_loaded<Cfg>(
+        acc, t, t.M, t.N,
+        [&](int row, int col) EE_ALWAYS_INLINE { return to_f32(p.Hg[static_cast<int64_t>(row) * p.ld + col]); },
+        [&](int row, int col, int, float hu, float hg) EE_ALWAYS_INLINE {
+          if (row < t.M && col < t.N) {
+            const int64_t o = static_cast<int64_t>(row) * p.ld + col;
+            p.Hu[o] = from_f32<T>(hu);
+            p.A[o] = from_f32<T>(silu_f(hg) * hu);
+          }
+        });
   }
 };
 
@@ -226,25 +230,21 @@ struct EpiSwiGLUBwd {
     T *dHu;
     int64_t ld;
   };
-  __device__ static void apply(const Params &p, f32x16_t (&acc)[2][2], const TileCtx &t) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = t.row(i, v);
-        if (row >= t.M) continue;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int col = t.col(j);
-          if (col >= t.N) continue;
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    for_each_acc_loaded<Cfg>(
+        acc, t, t.M, t.N,
+        [&](int row, int col) EE_ALWAYS_INLINE {
           const int64_t o = static_cast<int64_t>(row) * p.ld + col;
-          const float da = acc[i][j][v];
-          const float hg = to_f32(p.Hg[o]);
-          const float hu = to_f32(p.Hu[o]);
-          p.dHg[o] = from_f32<T>(da * hu * silu_grad_f(hg));
-          p.dHu[o] = from_f32<T>(da * silu_f(hg));
-        }
-      }
+          return F2{to_f32(p.Hg[o]), to_f32(p.Hu[o])};
+        },
+        [&](int row, int col, int, float da, F2 h) EE_ALWAYS_INLINE {
+          if (row < t.M && col < t.N) {
+            const int64_t o = static_cast<int64_t>(row) * p.ld + col;
+            p.dHg[o] = from_f32<T>(da * h.b * silu_grad_f(h.a));
+            p.dHu[o] = from_f32<T>(da * silu_f(h.a));
+          }
+        });
   }
 };
 

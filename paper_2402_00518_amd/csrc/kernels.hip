@@ -3,6 +3,8 @@
 // instantiations with their fused epilogues.
 #include <math.h>
 
+#include <type_traits>
+
 #include "epilogues.h"
 #include "launch.h"
 
@@ -163,51 +165,63 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, const fl
 }
 
 // ---------------------------------------------------------- cross-entropy
+// 32 tokens x 8 groups of vocab tiles per block: each thread merges the
+// (max, sum-exp) partials of every 8th tile online, then the 8 groups are
+// merged in a fixed order.
+__device__ __forceinline__ void lse_merge(float &m, float &l, float m2, float l2) {
+  const float mn = fmaxf(m, m2);
+  l = l * expf(m - mn) + l2 * expf(m2 - mn);
+  m = mn;
+}
+
 __global__ __launch_bounds__(256) void ce_reduce_kernel(CeReduceArgs a) {
-  __shared__ float red[256];
-  const int n = blockIdx.x * 256 + threadIdx.x;
+  __shared__ float sm_m[8][32], sm_l[8][32];
+  const int tk = threadIdx.x & 31, tg = threadIdx.x >> 5;
+  const int n = blockIdx.x * 32 + tk;
+  float m = -INFINITY, l = 0.0f;
+  if (n < a.n) {
+    for (int t = tg; t < a.tiles; t += 8) {
+      const int64_t o = static_cast<int64_t>(t) * a.ldn + n;
+      lse_merge(m, l, a.part_m[o], a.part_l[o]);
+    }
+  }
+  sm_m[tg][tk] = m;
+  sm_l[tg][tk] = l;
+  __syncthreads();
+  if (tg != 0) return;
   float contrib = 0.0f;
   if (n < a.n) {
-    float mx = -INFINITY;
-    for (int t = 0; t < a.tiles; ++t) mx = fmaxf(mx, a.part_m[static_cast<int64_t>(t) * a.ldn + n]);
-    float l = 0.0f;
-    for (int t = 0; t < a.tiles; ++t) {
-      const int64_t o = static_cast<int64_t>(t) * a.ldn + n;
-      l += a.part_l[o] * expf(a.part_m[o] - mx);
-    }
-    const float lse = mx + logf(l);
+    m = sm_m[0][tk];
+    l = sm_l[0][tk];
+    for (int g = 1; g < 8; ++g) lse_merge(m, l, sm_m[g][tk], sm_l[g][tk]);
+    const float lse = m + logf(l);
     const int y = a.targets[n];
     const bool ok = y >= 0 && y < a.vocab;
     if (!ok) *a.flag = 1;
     const float nll = ok ? lse - a.tgt[n] : NAN;
     float w = a.token_w != nullptr ? a.token_w[n] : 1.0f;
-    if (a.dynamic_weights) w *= expf(mx - lse);  // detached confidence = max probability
-    const float s = a.exit_weight * w / static_cast<float>(a.n);
-    a.sn[n] = s;
-    for (int t = 0; t < a.tiles; ++t) {
-      const int64_t o = static_cast<int64_t>(t) * a.ldn + n;
-      a.part_m[o] = s * expf(a.part_m[o] - lse);
-    }
+    if (a.dynamic_weights) w *= expf(m - lse);  // detached confidence = max probability
+    a.lse[n] = lse;
+    a.sn[n] = a.exit_weight * w / static_cast<float>(a.n);
     if (a.row_loss != nullptr) a.row_loss[n] = nll;
     contrib = w * nll;
   }
-  red[threadIdx.x] = contrib;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) a.block_sums[blockIdx.x] = red[0];
+#pragma unroll
+  for (int o = 16; o > 0; o >>= 1) contrib += __shfl_xor(contrib, o, 32);
+  if (tk == 0) a.block_sums[blockIdx.x] = contrib;
 }
 
-// In-place seed: each thread owns 8 consecutive tokens of 16 vocab rows.
+// In-place seed: each thread owns 8 consecutive tokens of 16 vocab rows (one
+// vocab tile).  coef = s_n exp(m_tile - LSE_n) turns the stored
+// exp(S - m_tile) into s_n softmax(S); the target entry loses s_n.
 template <typename T>
-__global__ __launch_bounds__(256) void seed_kernel(T *P, const float *coef, const float *sn,
-                                                   const int32_t *targets, int n, int ldn, int vocab) {
-  const int c0 = blockIdx.x * 2048 + threadIdx.x * 8;
+__global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, const float *lse,
+                                                   const float *sn, const int32_t *targets, int n,
+                                                   int ldn, int vocab, int vtile) {
+  const int c0 = blockIdx.y * 2048 + threadIdx.x * 8;
   if (c0 >= ldn) return;
-  const int v0 = blockIdx.y * 16;
-  const int tile = v0 / kVocabTile;
+  const int v0 = blockIdx.x * 16;
+  const int tile = v0 / vtile;
   float cf[8], s[8];
   int yy[8];
   bool ok[8];
@@ -215,19 +229,30 @@ __global__ __launch_bounds__(256) void seed_kernel(T *P, const float *coef, cons
   for (int e = 0; e < 8; ++e) {
     const int c = c0 + e;
     ok[e] = c < n;
-    cf[e] = ok[e] ? coef[static_cast<int64_t>(tile) * ldn + c] : 0.0f;
     s[e] = ok[e] ? sn[c] : 0.0f;
+    cf[e] = ok[e] ? s[e] * expf(part_m[static_cast<int64_t>(tile) * ldn + c] - lse[c]) : 0.0f;
     yy[e] = ok[e] ? targets[c] : -1;
   }
-  for (int r = 0; r < 16; ++r) {
-    const int v = v0 + r;
-    if (v >= vocab) break;
-    T *row = P + static_cast<int64_t>(v) * ldn + c0;
-    float p[8], g[8];
-    load_f32<8>(row, p);
+  const int rows = min(16, vocab - v0);
+  // Issue every row's load before the first store (raw 16- or 32-byte
+  // vectors; converted at use).
+  constexpr int VEC = 8 * sizeof(T) / 16;  // 16-byte vectors per 8 values
+  u32x4_t raw[16][VEC];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) g[e] = ok[e] ? p[e] * cf[e] - (yy[e] == v ? s[e] : 0.0f) : 0.0f;
-    store_f32<8>(row, g);
+  for (int r = 0; r < 16; ++r) {
+    const u32x4_t *src = reinterpret_cast<const u32x4_t *>(P + static_cast<int64_t>(v0 + min(r, rows - 1)) * ldn + c0);
+#pragma unroll
+    for (int q = 0; q < VEC; ++q) raw[r][q] = src[q];
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    if (r < rows) {
+      float p[8], g[8];
+      load_f32<8>(reinterpret_cast<const T *>(raw[r]), p);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) g[e] = ok[e] ? p[e] * cf[e] - (yy[e] == v0 + r ? s[e] : 0.0f) : 0.0f;
+      store_f32<8>(P + static_cast<int64_t>(v0 + r) * ldn + c0, g);
+    }
   }
 }
 
@@ -249,14 +274,23 @@ __global__ __launch_bounds__(256) void final_loss_kernel(const float *bs, int nb
   }
 }
 
+// 32 columns x 8 groups of tiles per block; groups merge in a fixed order.
 __global__ __launch_bounds__(256) void gain_reduce_kernel(const float *pa, int ta, const float *pb, int tb,
                                                           int h, float *out, int accumulate) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= h) return;
+  __shared__ float red[8][32];
+  const int c = threadIdx.x & 31, g = threadIdx.x >> 5;
+  const int j = blockIdx.x * 32 + c;
   float s = 0.0f;
-  for (int t = 0; t < ta; ++t) s += pa[static_cast<int64_t>(t) * h + j];
-  for (int t = 0; t < tb; ++t) s += pb[static_cast<int64_t>(t) * h + j];
-  out[j] = accumulate ? out[j] + s : s;
+  if (j < h) {
+    for (int t = g; t < ta; t += 8) s += pa[static_cast<int64_t>(t) * h + j];
+    for (int t = g; t < tb; t += 8) s += pb[static_cast<int64_t>(t) * h + j];
+  }
+  red[g][c] = s;
+  __syncthreads();
+  if (g != 0 || j >= h) return;
+  float total = red[0][c];
+  for (int k = 1; k < 8; ++k) total += red[k][c];
+  out[j] = accumulate ? out[j] + total : total;
 }
 
 __global__ void clear_flag_kernel(int *flag) { *flag = 0; }
@@ -303,15 +337,15 @@ hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, c
 }
 
 hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream) {
-  hipLaunchKernelGGL(ce_reduce_kernel, dim3(cdiv(a.n, 256)), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(ce_reduce_kernel, dim3(cdiv(a.n, 32)), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
-hipError_t launch_seed(bool f32, void *P, const float *coef, const float *sn, const int32_t *targets, int n,
-                       int ldn, int vocab, hipStream_t stream) {
-  const dim3 grid(cdiv(ldn, 2048), cdiv(vocab, 16));
-  EE_DISPATCH(f32, hipLaunchKernelGGL(seed_kernel<T>, grid, dim3(256), 0, stream, static_cast<T *>(P), coef,
-                                      sn, targets, n, ldn, vocab));
+hipError_t launch_seed(bool f32, void *P, const float *part_m, const float *lse, const float *sn,
+                       const int32_t *targets, int n, int ldn, int vocab, int vtile, hipStream_t stream) {
+  const dim3 grid(cdiv(vocab, 16), cdiv(ldn, 2048));
+  EE_DISPATCH(f32, hipLaunchKernelGGL(seed_kernel<T>, grid, dim3(256), 0, stream, static_cast<T *>(P), part_m,
+                                      lse, sn, targets, n, ldn, vocab, vtile));
   return hipGetLastError();
 }
 
@@ -324,7 +358,7 @@ hipError_t launch_final_loss(const float *block_sums, int blocks, int n, float *
 
 hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *part_b, int tiles_b, int h,
                               float *out, int accumulate, hipStream_t stream) {
-  hipLaunchKernelGGL(gain_reduce_kernel, dim3(cdiv(h, 256)), dim3(256), 0, stream, part_a, tiles_a, part_b,
+  hipLaunchKernelGGL(gain_reduce_kernel, dim3(cdiv(h, 32)), dim3(256), 0, stream, part_a, tiles_a, part_b,
                      tiles_b, h, out, accumulate);
   return hipGetLastError();
 }
@@ -342,11 +376,25 @@ hipError_t launch_clear_flag(int *flag, hipStream_t stream) {
 }
 
 // ------------------------------------------------------------------ GEMMs
+// bf16 GEMMs whose operands are both K-major take the 256 x 256 tile; the
+// others (fp32, or a transposed operand) the 128 x 128 tile.
+template <typename T, bool AK, bool BKM, class Epi>
+hipError_t run_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Params &ep, hipStream_t stream) {
+  if constexpr (std::is_same<T, bf16_t>::value && AK && BKM)
+    return launch_gemm<T, AK, BKM, Epi, CfgBig>(A, B, s, ep, stream);
+  else
+    return launch_gemm<T, AK, BKM, Epi, CfgSmall>(A, B, s, ep, stream);
+}
+
+int gemm_tile_rows(bool f32, bool a_kmajor, bool b_kmajor) {
+  return (!f32 && a_kmajor && b_kmajor) ? CfgBig::BM : CfgSmall::BM;
+}
+
 hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, int n, int h, void *P, int ldn,
                        float *part_m, float *part_l, float *tgt, const int32_t *targets, hipStream_t stream) {
   EE_DISPATCH(f32, {
     typename EpiLogits<T>::Params ep{static_cast<T *>(P), ldn, part_m, part_l, tgt, targets};
-    return launch_gemm<T, true, true, EpiLogits<T>>(Operand{w_out, h}, Operand{z, h}, GemmShape{vocab, n, h}, ep,
+    return run_gemm<T, true, true, EpiLogits<T>>(Operand{w_out, h}, Operand{z, h}, GemmShape{vocab, n, h}, ep,
                                                     stream);
   });
   return hipSuccess;
@@ -358,7 +406,7 @@ hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, in
   EE_DISPATCH(f32, {
     typename EpiWeightGrad<T>::Params ep{dw, h, static_cast<const T *>(gain), static_cast<const T *>(w), part,
                                          accumulate};
-    return launch_gemm<T, true, true, EpiWeightGrad<T>>(Operand{g_t, ldn}, Operand{xhat_t, ldn},
+    return run_gemm<T, true, true, EpiWeightGrad<T>>(Operand{g_t, ldn}, Operand{xhat_t, ldn},
                                                         GemmShape{m, h, ldn}, ep, stream);
   });
   return hipSuccess;
@@ -370,7 +418,7 @@ hipError_t gemm_weight_grad_mn(bool f32, const void *g, const void *xhat, int m,
   EE_DISPATCH(f32, {
     typename EpiWeightGrad<T>::Params ep{dw, h, static_cast<const T *>(gain), static_cast<const T *>(w), part,
                                          accumulate};
-    return launch_gemm<T, false, false, EpiWeightGrad<T>>(Operand{g, m}, Operand{xhat, h}, GemmShape{m, h, n},
+    return run_gemm<T, false, false, EpiWeightGrad<T>>(Operand{g, m}, Operand{xhat, h}, GemmShape{m, h, n},
                                                           ep, stream);
   });
   return hipSuccess;
@@ -380,7 +428,7 @@ hipError_t gemm_gate(bool f32, const void *u, const void *w_gate, int n, int int
                      hipStream_t stream) {
   EE_DISPATCH(f32, {
     typename EpiStoreT<T>::Params ep{static_cast<T *>(hg), inter};
-    return launch_gemm<T, true, true, EpiStoreT<T>>(Operand{u, h}, Operand{w_gate, h}, GemmShape{n, inter, h},
+    return run_gemm<T, true, true, EpiStoreT<T>>(Operand{u, h}, Operand{w_gate, h}, GemmShape{n, inter, h},
                                                     ep, stream);
   });
   return hipSuccess;
@@ -391,7 +439,7 @@ hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int 
   EE_DISPATCH(f32, {
     typename EpiSwiGLU<T>::Params ep{static_cast<const T *>(hg), static_cast<T *>(hu), static_cast<T *>(act),
                                      inter};
-    return launch_gemm<T, true, true, EpiSwiGLU<T>>(Operand{u, h}, Operand{w_up, h}, GemmShape{n, inter, h}, ep,
+    return run_gemm<T, true, true, EpiSwiGLU<T>>(Operand{u, h}, Operand{w_up, h}, GemmShape{n, inter, h}, ep,
                                                     stream);
   });
   return hipSuccess;
@@ -401,7 +449,7 @@ hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, con
                               int inter, float *y, hipStream_t stream) {
   EE_DISPATCH(f32, {
     typename EpiStoreF32<T>::Params ep{y, h, static_cast<const T *>(x), h, n, 0};
-    return launch_gemm<T, true, true, EpiStoreF32<T>>(Operand{act, inter}, Operand{w_down, inter},
+    return run_gemm<T, true, true, EpiStoreF32<T>>(Operand{act, inter}, Operand{w_down, inter},
                                                       GemmShape{n, h, inter}, ep, stream);
   });
   return hipSuccess;
@@ -411,7 +459,7 @@ hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn,
                    hipStream_t stream) {
   EE_DISPATCH(f32, {
     typename EpiStoreF32<T>::Params ep{dz, h, nullptr, 0, n, 0};
-    return launch_gemm<T, false, false, EpiStoreF32<T>>(Operand{g_t, ldn}, Operand{w_out, h},
+    return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{g_t, ldn}, Operand{w_out, h},
                                                         GemmShape{ldn, h, vocab}, ep, stream);
   });
   return hipSuccess;
@@ -422,7 +470,7 @@ hipError_t gemm_da_swiglu(bool f32, const void *dy, const void *w_down, int n, i
   EE_DISPATCH(f32, {
     typename EpiSwiGLUBwd<T>::Params ep{static_cast<const T *>(hg), static_cast<const T *>(hu),
                                         static_cast<T *>(dhg), static_cast<T *>(dhu), inter};
-    return launch_gemm<T, true, false, EpiSwiGLUBwd<T>>(Operand{dy, h}, Operand{w_down, inter},
+    return run_gemm<T, true, false, EpiSwiGLUBwd<T>>(Operand{dy, h}, Operand{w_down, inter},
                                                         GemmShape{n, inter, h}, ep, stream);
   });
   return hipSuccess;
@@ -432,7 +480,7 @@ hipError_t gemm_dw_down(bool f32, const void *dy, const void *act, int n, int h,
                         int accumulate, hipStream_t stream) {
   EE_DISPATCH(f32, {
     typename EpiStoreF32<T>::Params ep{dwd, inter, nullptr, 0, h, accumulate};
-    return launch_gemm<T, false, false, EpiStoreF32<T>>(Operand{dy, h}, Operand{act, inter},
+    return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{dy, h}, Operand{act, inter},
                                                         GemmShape{h, inter, n}, ep, stream);
   });
   return hipSuccess;

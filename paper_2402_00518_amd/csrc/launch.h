@@ -8,9 +8,11 @@
 
 namespace ee {
 
-// Tile sizes the workspace layout depends on.
-constexpr int kVocabTile = 128;   // rows of a GEMM output tile
 constexpr int kTokenPad = 64;     // padding of the token dimension
+
+// Rows of the output tile of the GEMM for this dtype and operand layout (the
+// softmax and gain-gradient partials come one per tile row-block).
+int gemm_tile_rows(bool f32, bool a_kmajor, bool b_kmajor);
 
 // Row-wise RMSNorm scale r[n] = (mean_j x[n][j]^2 + eps)^(-1/2).
 hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps,
@@ -23,18 +25,18 @@ hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, c
                              const void *gain, int n, int ldn, int h, void *z, void *x_hat,
                              void *x_hat_t, hipStream_t stream);
 
-// Combine the per-tile softmax partials of each token into LSE, the row NLL,
-// the loss-weight s_n and the per-tile seed coefficients (written over
-// part_m).  Also flags targets outside [0, V).
+// Combine the per-tile softmax partials of each token into LSE, the row NLL
+// and the loss weight s_n.  Also flags targets outside [0, V).
 struct CeReduceArgs {
-  float *part_m;          // in: tile max; out: s_n * exp(m_tile - LSE)
+  const float *part_m;
   const float *part_l;
   const float *tgt;
   const int32_t *targets;
   const float *token_w;   // or NULL
-  float *sn;              // [ldn] s_n
+  float *lse;             // [ldn] log-sum-exp
+  float *sn;              // [ldn] s_n = w_e m_n / N
   float *row_loss;        // [n] or NULL
-  float *block_sums;      // [cdiv(n, 256)]
+  float *block_sums;      // [cdiv(n, 32)]
   int *flag;
   int n, ldn, vocab, tiles;
   float exit_weight;
@@ -42,9 +44,10 @@ struct CeReduceArgs {
 };
 hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream);
 
-// In place: G[v][n] = P[v][n] * coef[v / 128][n] - (v == y_n) * s_n  (0 for n >= N).
-hipError_t launch_seed(bool f32, void *P, const float *coef, const float *sn, const int32_t *targets,
-                       int n, int ldn, int vocab, hipStream_t stream);
+// In place: G[v][n] = P[v][n] * s_n exp(m[v / vtile][n] - LSE_n) - (v == y_n) * s_n
+// (0 for n >= N).
+hipError_t launch_seed(bool f32, void *P, const float *part_m, const float *lse, const float *sn,
+                       const int32_t *targets, int n, int ldn, int vocab, int vtile, hipStream_t stream);
 
 // loss[0] = sum(block_sums) / n;  total[0] = (first ? 0 : total[0]) + w * loss[0].
 hipError_t launch_final_loss(const float *block_sums, int blocks, int n, float *loss, float *total,
