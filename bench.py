@@ -14,7 +14,6 @@ Prints one JSON line on stdout; progress goes to stderr.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -61,18 +60,11 @@ def step_flops(w):
     return per * N * w.n_exits
 
 
-def source_digest():
-    d = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2402_00518_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".h", ".hip", ".cpp")):
-            d.update(open(os.path.join(csrc, f), "rb").read())
-    return d.hexdigest()[:16]
-
-
 def measured_traffic(workload, kernel):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel sources; else None."""
+    """HBM bytes per launch (read + write, copy-calibrated) from committed
+    rocprofv3 counter runs, if they were taken on the current kernel sources;
+    else None."""
+    from paper_2402_00518_amd.traffic import source_digest
     try:
         data = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
@@ -81,6 +73,18 @@ def measured_traffic(workload, kernel):
     if not rec or rec.get("source_digest") != source_digest():
         return None
     return rec.get("bytes_per_launch")
+
+
+def copy_calibration(mib, copies=3):
+    """Plain device-to-device copies of a known size; a counter run over the
+    bench reads them to calibrate FETCH_SIZE and WRITE_SIZE."""
+    import torch
+    src = torch.ones(mib << 18, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(copies):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy calibration: {copies} copies of {mib} MiB")
 
 
 def cpu_baseline(batch, sample_tokens):
@@ -118,6 +122,8 @@ def main():
                     help="tokens of the batch the oracle runs on (0: all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-pass", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the step, copy a buffer of this size 3 times (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -202,6 +208,9 @@ def main():
                                "traffic": measured_traffic(w.name, dom),
                                "flops_per_launch": f, "avg_ms": kernels[dom]["avg_ms"]}
         log(f"dominant kernel {dom}: {kernels[dom]['avg_ms']:.4f} ms")
+
+    if args.copy_calibration_mib > 0:
+        copy_calibration(args.copy_calibration_mib)
 
     if not args.no_cpu_baseline:
         log("cpu baseline: oracle on the batch ...")

@@ -34,6 +34,17 @@ __device__ __forceinline__ void static_for(F &&f) {
   static_for_impl(static_cast<F &&>(f), std::make_integer_sequence<int, N>{});
 }
 
+// f(integral_constant<bool, a>) for a runtime flag a that is uniform across
+// the wave: the branch is taken once, outside f, so the loads inside f are
+// never predicated one by one (a predicated load ends in a full vmcnt wait).
+template <class F>
+__device__ __forceinline__ void with_flag(bool a, F &&f) {
+  if (a)
+    f(std::true_type{});
+  else
+    f(std::false_type{});
+}
+
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }

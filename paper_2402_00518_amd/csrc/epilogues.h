@@ -122,24 +122,33 @@ struct EpiWeightGrad {
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
     constexpr int NB = Cfg::NB;
     float g[NB], dg[NB];
-    static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
-      const int col = t.col(j);
-      g[j] = (p.gain != nullptr && col < t.N) ? to_f32(p.gain[col]) : 1.0f;
-      dg[j] = 0.0f;
+    with_flag(p.gain != nullptr, [&](auto G_) EE_ALWAYS_INLINE {
+      static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
+        g[j] = decltype(G_)::value ? to_f32(p.gain[min(t.col(j), t.N - 1)]) : 1.0f;
+        dg[j] = 0.0f;
+      });
     });
     const bool with_w = p.W != nullptr;
-    for_each_acc_loaded<Cfg>(
-        acc, t, t.M, t.N,
-        [&](int row, int col) EE_ALWAYS_INLINE {
-          const int64_t o = static_cast<int64_t>(row) * p.ldw + col;
-          return F2{with_w ? to_f32(p.W[o]) : 0.0f, p.accumulate ? p.dW[o] : 0.0f};
-        },
-        [&](int row, int col, int j, float c, F2 in) EE_ALWAYS_INLINE {
-          if (row < t.M && col < t.N) {
-            p.dW[static_cast<int64_t>(row) * p.ldw + col] = in.b + c * g[j];
-            dg[j] += in.a * c;
-          }
-        });
+    with_flag(with_w, [&](auto W_) EE_ALWAYS_INLINE {
+      with_flag(p.accumulate != 0, [&](auto A_) EE_ALWAYS_INLINE {
+        constexpr bool kW = decltype(W_)::value, kAcc = decltype(A_)::value;
+        for_each_acc_loaded<Cfg>(
+            acc, t, t.M, t.N,
+            [&](int row, int col) EE_ALWAYS_INLINE {
+              const int64_t o = static_cast<int64_t>(row) * p.ldw + col;
+              F2 r{0.0f, 0.0f};
+              if constexpr (kW) r.a = to_f32(p.W[o]);
+              if constexpr (kAcc) r.b = p.dW[o];
+              return r;
+            },
+            [&](int row, int col, int j, float c, F2 in) EE_ALWAYS_INLINE {
+              if (row < t.M && col < t.N) {
+                p.dW[static_cast<int64_t>(row) * p.ldw + col] = in.b + c * g[j];
+                if constexpr (kW) dg[j] += in.a * c;
+              }
+            });
+      });
+    });
     if (with_w) {
       tile_col_reduce<false, Cfg>(t, dg);
       if (t.wave_m == 0 && t.lane < 32) {
@@ -166,17 +175,28 @@ struct EpiStoreF32 {
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc_loaded<Cfg>(
-        acc, t, p.rows, t.N,
-        [&](int row, int col) EE_ALWAYS_INLINE {
-          float r = 0.0f;
-          if (p.residual != nullptr) r += to_f32(p.residual[static_cast<int64_t>(row) * p.ldr + col]);
-          if (p.accumulate) r += p.C[static_cast<int64_t>(row) * p.ldc + col];
-          return r;
-        },
-        [&](int row, int col, int, float a, float in) EE_ALWAYS_INLINE {
-          if (row < p.rows && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = a + in;
-        });
+    with_flag(p.residual != nullptr, [&](auto R_) EE_ALWAYS_INLINE {
+      with_flag(p.accumulate != 0, [&](auto A_) EE_ALWAYS_INLINE {
+        constexpr bool kRes = decltype(R_)::value, kAcc = decltype(A_)::value;
+        if constexpr (!kRes && !kAcc) {
+          for_each_acc<Cfg>(acc, t, [&](int row, int col, int, float a) EE_ALWAYS_INLINE {
+            if (row < p.rows && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = a;
+          });
+        } else {
+          for_each_acc_loaded<Cfg>(
+              acc, t, p.rows, t.N,
+              [&](int row, int col) EE_ALWAYS_INLINE {
+                float r = 0.0f;
+                if constexpr (kRes) r += to_f32(p.residual[static_cast<int64_t>(row) * p.ldr + col]);
+                if constexpr (kAcc) r += p.C[static_cast<int64_t>(row) * p.ldc + col];
+                return r;
+              },
+              [&](int row, int col, int, float a, float in) EE_ALWAYS_INLINE {
+                if (row < p.rows && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = a + in;
+              });
+        }
+      });
+    });
   }
 };
 

@@ -1,0 +1,142 @@
+"""HBM traffic per kernel launch from rocprofv3 counter runs.
+
+Two counter runs of the same bench command give, per dispatch, FETCH_SIZE
+(KiB read past L2) and WRITE_SIZE (KiB written past L2).  The bench command
+also copies a buffer of known size a few times (``bench.py
+--copy-calibration-mib M``); what the counters read for that plain copy
+calibrates them: scaled bytes = counter bytes * known bytes / copy's counter
+bytes, separately for reads and writes.
+
+    python -m paper_2402_00518_amd.traffic --workload llama7b_norm \\
+        --fetch DIR_A/run_counter_collection.csv --write DIR_B/run_counter_collection.csv \\
+        --copy-bytes 1073741824 --command "..."
+
+updates ``profiles/traffic.json``.  The figures are tied to a digest of the
+kernel sources; bench.py reports them only while the sources are unchanged.
+"""
+
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+from collections import defaultdict
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+# Profiling label -> (substring of the demangled kernel name, slot).  Kernels
+# that share one instantiation within an exit's step alternate in launch
+# order (dZ before the down-projection gradient, gate before up gradient):
+# slot = index of the launch modulo 2 among that instantiation's launches.
+LABEL_KERNELS = {
+    "logits + softmax partials": ("ee::EpiLogits<", None),
+    "output-matrix gradient": ("true, true, ee::EpiWeightGrad<", None),
+    "dZ": ("false, false, ee::EpiStoreF32<", 0),
+    "down gradient": ("false, false, ee::EpiStoreF32<", 1),
+    "gate gradient": ("false, false, ee::EpiWeightGrad<", 0),
+    "up gradient": ("false, false, ee::EpiWeightGrad<", 1),
+    "gate projection": ("ee::EpiStoreT<", None),
+    "up projection + swiglu": ("ee::EpiSwiGLU<", None),
+    "down projection + residual": ("true, true, ee::EpiStoreF32<", None),
+    "dA + swiglu backward": ("ee::EpiSwiGLUBwd<", None),
+    "logit seed": ("seed_kernel", None),
+    "cross-entropy reduce": ("ce_reduce_kernel", None),
+}
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def source_digest() -> str:
+    """Digest of the HIP/C++ sources of the library (kernels and ABI)."""
+    d = hashlib.sha256()
+    csrc = os.path.join(PKG, "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".h", ".hip", ".cpp")):
+            d.update(open(os.path.join(csrc, f), "rb").read())
+    return d.hexdigest()[:16]
+
+
+def read_counter(path: str, counter: str):
+    """[(dispatch id, kernel name, value in KiB)] for one counter, in dispatch order."""
+    rows = []
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter:
+                rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+    rows.sort()
+    return rows
+
+
+def copy_factor(rows, copy_bytes: int, copies: int) -> tuple[float, float]:
+    """Known bytes / counter bytes of the calibration copies (the `copies`
+    largest copy dispatches), and their mean counter KiB."""
+    vals = sorted((v for _, name, v in rows if COPY_KERNEL in name), reverse=True)[:copies]
+    if len(vals) < copies:
+        raise SystemExit(f"found {len(vals)} copy dispatches, expected {copies}")
+    kib = sum(vals) / len(vals)
+    return copy_bytes / (kib * 1024.0), kib
+
+
+def per_label(rows):
+    """Mean counter KiB per dispatch for every label of LABEL_KERNELS."""
+    seen = defaultdict(int)
+    acc = defaultdict(list)
+    for _, name, v in rows:
+        for label, (pat, slot) in LABEL_KERNELS.items():
+            if pat not in name:
+                continue
+            if slot is None:
+                acc[label].append(v)
+            else:
+                if seen[pat] % 2 == slot:
+                    acc[label].append(v)
+        for pat in {p for p, s in LABEL_KERNELS.values() if s is not None}:
+            if pat in name:
+                seen[pat] += 1
+    return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--workload", required=True)
+    ap.add_argument("--fetch", required=True, help="counter_collection.csv of the FETCH_SIZE run")
+    ap.add_argument("--write", required=True, help="counter_collection.csv of the WRITE_SIZE run")
+    ap.add_argument("--copy-bytes", type=int, required=True)
+    ap.add_argument("--copies", type=int, default=3)
+    ap.add_argument("--command", default="", help="the rocprofv3 commands, recorded with the figures")
+    ap.add_argument("--out", default=TRAFFIC_FILE)
+    args = ap.parse_args()
+
+    fr = read_counter(args.fetch, "FETCH_SIZE")
+    wr = read_counter(args.write, "WRITE_SIZE")
+    ff, fkib = copy_factor(fr, args.copy_bytes, args.copies)
+    wf, wkib = copy_factor(wr, args.copy_bytes, args.copies)
+    fl, wl = per_label(fr), per_label(wr)
+    try:
+        data = json.load(open(args.out))
+    except (OSError, ValueError):
+        data = {}
+    digest = source_digest()
+    data.setdefault("copy_calibration", {})[args.workload] = {
+        "copy_bytes": args.copy_bytes, "fetch_kib": fkib, "write_kib": wkib,
+        "fetch_factor": ff, "write_factor": wf}
+    rec = data.setdefault(args.workload, {})
+    for label in sorted(set(fl) & set(wl)):
+        fb = fl[label][0] * 1024.0 * ff
+        wb = wl[label][0] * 1024.0 * wf
+        rec[label] = {"fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                      "bytes_per_launch": fb + wb, "dispatches": fl[label][1],
+                      "source_digest": digest, "command": args.command}
+        print(f"{label:28s} read {fb / 1e6:10.2f} MB  write {wb / 1e6:10.2f} MB  ({fl[label][1]} dispatches)")
+    print(f"copy calibration: read factor {ff:.4f}, write factor {wf:.4f}")
+    os.makedirs(os.path.dirname(args.out), exist_ok=True)
+    with open(args.out, "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
+        f.write("\n")
+
+
+if __name__ == "__main__":
+    main()
