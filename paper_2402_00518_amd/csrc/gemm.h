@@ -80,10 +80,20 @@ __host__ __device__ constexpr int cdiv(int64_t a, int64_t b) { return static_cas
 // Byte offset of 16-byte chunk `ch` (0..7) of LDS tile row `row`.  A
 // ds_read_b128 is served 16 lanes at a time from 256 bytes of banks, i.e.
 // two 128-byte tile rows; the 16 lanes of a fragment read read 16
-// consecutive rows at one logical chunk, so rows of equal parity must land
-// on distinct chunks: the XOR key is (row / 2) mod 8.
+// consecutive rows at one logical chunk, so within every aligned group of 16
+// rows, rows of equal parity must land on distinct chunks: the XOR key's
+// bits come from row / 2.  That key repeats every 16 rows, so a lane's
+// fragment rows 32 apart share one swizzle and their addresses differ by a
+// constant.  Tiles written by the MN-major bf16 loader, whose lanes write
+// rows 8 apart, fold row / 16 into the key as well (WIDE), which spreads
+// those writes over all chunks.
+template <bool WIDE>
+__device__ __forceinline__ int lds_key(int row) {
+  return WIDE ? ((row >> 1) ^ (row >> 4)) & 7 : (row >> 1) & 7;
+}
+template <bool WIDE = false>
 __device__ __forceinline__ int lds_off(int row, int ch) {
-  return row * kRowBytes + ((ch ^ ((row >> 1) & 7)) << 4);
+  return row * kRowBytes + ((ch ^ lds_key<WIDE>(row)) << 4);
 }
 
 // ---------------------------------------------------------------- loaders
@@ -131,13 +141,12 @@ struct KMajorLoader {
   }
 };
 
-// MN-major tile: BK k-rows x ROWS contiguous operand rows.  A thread loads
-// 4 consecutive k-rows of one 16-byte column group and writes them
+// MN-major tile: BK k-rows x ROWS contiguous operand rows, written
 // transposed (k contiguous) into LDS.
 template <typename T, int ROWS, int THREADS> struct MNMajorLoader;
 
-// Adapter giving the MN-major loaders the grouped interface: the whole stage
-// is loaded and stored by group 0.
+// Adapter giving the fp32 MN-major loader the grouped interface: the whole
+// stage is loaded and stored by group 0.
 template <typename T, int ROWS, int THREADS, int GROUPS>
 struct MNMajorLoaderGrouped : MNMajorLoader<T, ROWS, THREADS> {
   int rows_, K_, tid_;
@@ -156,41 +165,94 @@ struct MNMajorLoaderGrouped : MNMajorLoader<T, ROWS, THREADS> {
   }
 };
 
-template <int ROWS, int THREADS> struct MNMajorLoader<bf16_t, ROWS, THREADS> {
-  static constexpr int GROUPS = ROWS / 8;                 // 16-byte column groups
-  static constexpr int PER = (64 / 4) * GROUPS / THREADS;  // 4 x 8 blocks per thread
-  u32x4_t reg[PER][4];  // reg[p][r] = 8 values of k-row r
+// bf16, 64 k-rows x ROWS operand rows per stage, in blocks of 4 k-rows x 8
+// operand rows (one 16-byte load per k-row), one block per thread.  Inside
+// a wave, lane bits 0-2 pick 8 consecutive column groups (128 contiguous
+// bytes of one k-row per load) and bits 3-5 pick the k-block, so each load
+// instruction reads whole 128-byte lines.  A block becomes 8 LDS rows of 4 k
+// values (8 bytes); each ds_write_b64 writes the even rows of half the lanes
+// and the odd rows of the other half, which with the WIDE lds_key reaches
+// every bank.
+// The byte shuffles are v_perm_b32, whose per-lane selector also makes that
+// even/odd choice.  The whole stage is loaded and written in the first
+// substep: the writes need all four k-rows of a block, and loading them at
+// once gives each a full stage of latency.
+// K-rows past the end re-read the last k-row; with ZERO_TAIL they are
+// written to LDS as zeros.  One operand of a product zeroed is enough, so
+// only the A side pays for it.
+template <int ROWS, int THREADS, int GROUPS, bool ZERO_TAIL>
+struct MNMajorLoaderB16 {
+  static constexpr int MBW = ROWS / 64;  // 8-block column groups per tile
+  static_assert(16 * ROWS / 8 == THREADS, "one 4 x 8 block per thread");
+  u32x4_t reg[4];   // k-rows 0..3 of the block
+  uint32_t goff;    // byte offset of the block's first k-row in a stage's panel
+  int kr0;          // first k-row of the block inside the stage
+  int lim;          // last valid k-row of the block (relative), as of the last load
+  int K_;
+  int lbase;        // LDS byte offset of the block's first row (with the even/odd choice)
+  int c0;           // logical chunk XOR the rows' swizzle key (before the row pair index)
+  uint32_t sel_first;  // v_perm_b32 selector of the row written first
+  int dsec;             // byte distance from the first row written to the second
 
-  __device__ __forceinline__ void load(const bf16_t *base, int64_t ld, int row0, int rows,
-                                       int k0, int K, int tid) {
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int b = tid + p * THREADS;
-      const int kb = b / GROUPS, mb = b % GROUPS;
-      const int m = min(row0 + mb * 8, rows - 8);  // rows is a multiple of 8
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int k = k0 + kb * 4 + r;
-        const u32x4_t v = *reinterpret_cast<const u32x4_t *>(base + static_cast<int64_t>(min(k, K - 1)) * ld + m);
-        reg[p][r] = k < K ? v : u32x4_t{0, 0, 0, 0};
-      }
+  __device__ __forceinline__ void init(int64_t ld, int row0, int rows, int K, int tid) {
+    const int lane = tid & 63, wb = tid >> 6;
+    const int mb = (lane & 7) + 8 * (wb % MBW);
+    const int kb = (lane >> 3) + 8 * (wb / MBW);
+    const int mcol = min(row0 + mb * 8, rows - 8) - row0;  // rows is a multiple of 8
+    kr0 = kb * 4;
+    goff = static_cast<uint32_t>((static_cast<int64_t>(kr0) * ld + mcol) * 2);
+    K_ = K;
+    lim = 3;
+    const int sw = (lane >> 5) & 1;  // this lane writes the odd row of each pair first
+    // rows mb*8 + 2j + {0, 1} share lds_key = K0 ^ j (j < 4)
+    const int key0 = ((4 * (mb & 1)) ^ ((mb >> 1) & 7)) & 7;
+    c0 = (kb >> 1) ^ key0;
+    lbase = mb * 8 * kRowBytes + sw * kRowBytes + (kb & 1) * 8;
+    // v_perm_b32(x = k-row pair high, y = k-row pair low): even operand row
+    // takes the low 16 bits of both, odd operand row the high 16 bits.
+    sel_first = sw ? 0x07060302u : 0x05040100u;
+    dsec = sw ? -kRowBytes : kRowBytes;
+  }
+  template <int G>
+  __device__ __forceinline__ void load(const bf16_t *base, int64_t ld, int row0, int k0) {
+    if constexpr (G == 0) {
+      const char *panel = reinterpret_cast<const char *>(base + static_cast<int64_t>(k0) * ld + row0);
+      const int l = min(3, K_ - 1 - k0 - kr0);  // k-rows past K re-read the last one
+      // l < 0 when the whole block lies past K: the (negative) row offset
+      // then points back at k-row K - 1, and goff + offset stays >= 0.
+      const int ld2 = static_cast<int>(ld * 2);  // < 2^23, checked by the launcher
+      static_for<4>([&](auto r) EE_ALWAYS_INLINE {
+        const int rr = min(static_cast<int>(decltype(r)::value), l);
+        reg[r] = *reinterpret_cast<const u32x4_t *>(panel + (goff + static_cast<uint32_t>(__mul24(rr, ld2))));
+      });
+      if constexpr (ZERO_TAIL) lim = l;
     }
   }
-  __device__ __forceinline__ void store(char *lds, int tid) const {
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int b = tid + p * THREADS;
-      const int kb = b / GROUPS, mb = b % GROUPS;
-      const int ch = kb >> 1, half = (kb & 1) * 8;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {  // dword j holds columns 2j (low) and 2j+1 (high)
-        const uint32_t a0 = reg[p][0][j], a1 = reg[p][1][j], a2 = reg[p][2][j], a3 = reg[p][3][j];
-        const u32x2_t lo = {(a0 & 0xFFFFu) | (a1 << 16), (a2 & 0xFFFFu) | (a3 << 16)};
-        const u32x2_t hi = {(a0 >> 16) | (a1 & 0xFFFF0000u), (a2 >> 16) | (a3 & 0xFFFF0000u)};
-        const int row = mb * 8 + 2 * j;
-        *reinterpret_cast<u32x2_t *>(lds + lds_off(row, ch) + half) = lo;
-        *reinterpret_cast<u32x2_t *>(lds + lds_off(row + 1, ch) + half) = hi;
-      }
+  template <int G>
+  __device__ __forceinline__ void store(char *lds, int) const {
+    if constexpr (G == 0) {
+      u32x4_t a[4];
+      static_for<4>([&](auto r) EE_ALWAYS_INLINE {
+        constexpr int R = decltype(r)::value;
+        if constexpr (ZERO_TAIL) {
+          const bool ok = R <= lim;
+          static_for<4>([&](auto j) EE_ALWAYS_INLINE { a[R][decltype(j)::value] = ok ? reg[R][decltype(j)::value] : 0u; });
+        } else {
+          a[R] = reg[R];
+        }
+      });
+      static_for<4>([&](auto jj) EE_ALWAYS_INLINE {
+        constexpr int j = decltype(jj)::value;
+        // dword j of a k-row holds operand rows 2j (low half) and 2j+1 (high half)
+        const uint32_t sel_second = sel_first ^ 0x02020202u;  // the other half of each dword
+        const u32x2_t first = {__builtin_amdgcn_perm(a[1][j], a[0][j], sel_first),
+                               __builtin_amdgcn_perm(a[3][j], a[2][j], sel_first)};
+        const u32x2_t second = {__builtin_amdgcn_perm(a[1][j], a[0][j], sel_second),
+                                __builtin_amdgcn_perm(a[3][j], a[2][j], sel_second)};
+        const int off = lbase + j * 2 * kRowBytes + ((c0 ^ j) << 4);
+        *reinterpret_cast<u32x2_t *>(lds + off) = first;
+        *reinterpret_cast<u32x2_t *>(lds + off + dsec) = second;
+      });
     }
   }
 };
@@ -229,19 +291,23 @@ template <int ROWS, int THREADS> struct MNMajorLoader<float, ROWS, THREADS> {
   }
 };
 
-template <typename T, bool KMajor, int ROWS, int THREADS, int GROUPS> struct LoaderSel {
+template <typename T, bool KMajor, int ROWS, int THREADS, int GROUPS, bool ZERO_TAIL> struct LoaderSel {
   using type = KMajorLoader<T, ROWS, THREADS, GROUPS>;
 };
-template <typename T, int ROWS, int THREADS, int GROUPS> struct LoaderSel<T, false, ROWS, THREADS, GROUPS> {
-  using type = MNMajorLoaderGrouped<T, ROWS, THREADS, GROUPS>;
+template <int ROWS, int THREADS, int GROUPS, bool ZERO_TAIL> struct LoaderSel<float, false, ROWS, THREADS, GROUPS, ZERO_TAIL> {
+  using type = MNMajorLoaderGrouped<float, ROWS, THREADS, GROUPS>;
 };
+template <int ROWS, int THREADS, int GROUPS, bool ZERO_TAIL> struct LoaderSel<bf16_t, false, ROWS, THREADS, GROUPS, ZERO_TAIL> {
+  using type = MNMajorLoaderB16<ROWS, THREADS, GROUPS, ZERO_TAIL>;
+};
+
 
 // ------------------------------------------------------------ MFMA step
 // Fragments of one K substep (16 values of K) for the wave's MB x NB blocks
 // of 32 x 32, read from one LDS stage, and the MFMAs that consume them.
-template <typename T, class Cfg> struct Frags;
+template <typename T, class Cfg, bool A_WIDE, bool B_WIDE> struct Frags;
 
-template <class Cfg> struct Frags<bf16_t, Cfg> {
+template <class Cfg, bool A_WIDE, bool B_WIDE> struct Frags<bf16_t, Cfg, A_WIDE, B_WIDE> {
   static constexpr int MB = Cfg::MB, NB = Cfg::NB;
   static constexpr int SUBSTEPS = 4;  // 4 x 16 = 64 values of K per stage
   static constexpr int MMAS = MB * NB;  // MFMAs per substep
@@ -251,10 +317,10 @@ template <class Cfg> struct Frags<bf16_t, Cfg> {
                                        int lane, int s) {
     const int r = lane & 31, ch = s * 2 + (lane >> 5);
     static_for<MB>([&](auto i) EE_ALWAYS_INLINE {
-      a[i] = *reinterpret_cast<const bf16x8_t *>(a_lds + lds_off(a_row0 + i * 32 + r, ch));
+      a[i] = *reinterpret_cast<const bf16x8_t *>(a_lds + lds_off<A_WIDE>(a_row0 + i * 32 + r, ch));
     });
     static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
-      b[j] = *reinterpret_cast<const bf16x8_t *>(b_lds + lds_off(b_row0 + j * 32 + r, ch));
+      b[j] = *reinterpret_cast<const bf16x8_t *>(b_lds + lds_off<B_WIDE>(b_row0 + j * 32 + r, ch));
     });
   }
   __device__ __forceinline__ void mma(f32x16_t (&acc)[MB][NB]) const {
@@ -266,7 +332,8 @@ template <class Cfg> struct Frags<bf16_t, Cfg> {
   }
 };
 
-template <class Cfg> struct Frags<float, Cfg> {
+template <class Cfg, bool A_WIDE, bool B_WIDE> struct Frags<float, Cfg, A_WIDE, B_WIDE> {
+  static_assert(!A_WIDE && !B_WIDE, "fp32 tiles use the narrow swizzle");
   static constexpr int MB = Cfg::MB, NB = Cfg::NB;
   static constexpr int SUBSTEPS = 2;  // 2 x 16 = 32 values of K per stage
   static constexpr int MMAS = 8 * MB * NB;  // MFMAs per substep
@@ -371,10 +438,11 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
   const T *a_ptr = static_cast<const T *>(A.ptr);
   const T *b_ptr = static_cast<const T *>(B.ptr);
 
-  using F = Frags<T, Cfg>;
+  constexpr bool kB16 = std::is_same<T, bf16_t>::value;
+  using F = Frags<T, Cfg, kB16 && !AK, kB16 && !BKM>;
   constexpr int SUB = F::SUBSTEPS;
-  typename LoaderSel<T, AK, Cfg::BM, Cfg::THREADS, SUB>::type la;
-  typename LoaderSel<T, BKM, Cfg::BN, Cfg::THREADS, SUB>::type lb;
+  typename LoaderSel<T, AK, Cfg::BM, Cfg::THREADS, SUB, true>::type la;
+  typename LoaderSel<T, BKM, Cfg::BN, Cfg::THREADS, SUB, false>::type lb;
   la.init(A.ld, m0, s.M, s.K, tid);
   lb.init(B.ld, n0, s.N, s.K, tid);
   f32x16_t acc[MB][NB];
@@ -451,6 +519,8 @@ hipError_t launch_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Pa
   constexpr int BK = 8 * Elem<T>::CH;
   if (((AK || BKM) && s.K % BK != 0) || (!AK && s.M % 8 != 0) || (!BKM && s.N % 8 != 0))
     return hipErrorInvalidValue;  // shapes the loaders do not handle
+  if ((!AK && A.ld >= (int64_t{1} << 22)) || (!BKM && B.ld >= (int64_t{1} << 22)))
+    return hipErrorInvalidValue;  // MN-major loaders keep signed 24-bit k-row strides
   hipLaunchKernelGGL((gemm_kernel<T, AK, BKM, Epi, Cfg>), dim3(static_cast<unsigned>(blocks)),
                      dim3(Cfg::THREADS), 0, stream, A, B, s, ep);
   return hipGetLastError();

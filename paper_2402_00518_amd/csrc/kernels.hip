@@ -380,14 +380,16 @@ hipError_t launch_clear_flag(int *flag, hipStream_t stream) {
 // others (fp32, or a transposed operand) the 128 x 128 tile.
 template <typename T, bool AK, bool BKM, class Epi>
 hipError_t run_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Params &ep, hipStream_t stream) {
-  if constexpr (std::is_same<T, bf16_t>::value && AK && BKM)
+  if constexpr (std::is_same<T, bf16_t>::value)
     return launch_gemm<T, AK, BKM, Epi, CfgBig>(A, B, s, ep, stream);
   else
     return launch_gemm<T, AK, BKM, Epi, CfgSmall>(A, B, s, ep, stream);
 }
 
 int gemm_tile_rows(bool f32, bool a_kmajor, bool b_kmajor) {
-  return (!f32 && a_kmajor && b_kmajor) ? CfgBig::BM : CfgSmall::BM;
+  (void)a_kmajor;
+  (void)b_kmajor;
+  return f32 ? CfgSmall::BM : CfgBig::BM;
 }
 
 hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, int n, int h, void *P, int ldn,

@@ -109,6 +109,8 @@ SMALL_CASES = [
     ("norm_one_token", W.EXIT_NORM, 1, 64, 50, 0, "bf16", False),
     ("norm_vocab_one", W.EXIT_NORM, 37, 64, 1, 0, "bf16", False),
     ("norm_multi_tile", W.EXIT_NORM, 1000, 512, 2000, 0, "bf16", False),
+    # every MLP GEMM spans several 256-wide tiles with ragged M, N and K
+    ("mlp_multi_tile", W.EXIT_MLP, 600, 320, 1100, 704, "bf16", False),
 ]
 
 
