@@ -44,8 +44,53 @@ __device__ __forceinline__ void for_each_acc_loaded(f32x16_t (&acc)[Cfg::MB][Cfg
   });
 }
 
+// Row-vector form, for outputs stored transposed (C[m][n] at ptr[n*ld + m]):
+// a lane's accumulator rows 4q..4q+3 of a block are consecutive, so they
+// are one 8-byte (bf16) or 16-byte (fp32) access there.  f(row0, col, j,
+// vals, loaded) runs for every such group after all load(row0_c, col_c) of
+// the 32-row block have been issued (row0 and col clamped into the problem;
+// the row count must be a multiple of 4).
+template <class Cfg, class L, class F>
+__device__ __forceinline__ void for_each_acc4_loaded(f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t,
+                                                     L &&load, F &&f) {
+  using V = decltype(load(0, 0));
+  static_for<Cfg::MB>([&](auto i) EE_ALWAYS_INLINE {
+    V pre[4][Cfg::NB];
+    static_for<4>([&](auto q) EE_ALWAYS_INLINE {
+      const int row0 = min(t.row(i, 4 * q), t.M - 4);
+      static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE { pre[q][j] = load(row0, min(t.col(j), t.N - 1)); });
+    });
+    static_for<4>([&](auto q) EE_ALWAYS_INLINE {
+      constexpr int v0 = 4 * decltype(q)::value;
+      const int row0 = t.row(i, v0);
+      static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE {
+        const f32x4_t c = {acc[i][j][v0], acc[i][j][v0 + 1], acc[i][j][v0 + 2], acc[i][j][v0 + 3]};
+        f(row0, t.col(j), static_cast<int>(j), c, pre[q][j]);
+      });
+    });
+  });
+}
+
+// Four consecutive elements as fp32, and back.
+__device__ __forceinline__ f32x4_t load4(const float *p) { return *reinterpret_cast<const f32x4_t *>(p); }
+__device__ __forceinline__ f32x4_t load4(const bf16_t *p) {
+  const u32x2_t u = *reinterpret_cast<const u32x2_t *>(p);
+  return f32x4_t{__uint_as_float(u[0] << 16), __uint_as_float(u[0] & 0xFFFF0000u), __uint_as_float(u[1] << 16),
+                 __uint_as_float(u[1] & 0xFFFF0000u)};
+}
+__device__ __forceinline__ void store4(float *p, f32x4_t v) { *reinterpret_cast<f32x4_t *>(p) = v; }
+__device__ __forceinline__ void store4(bf16_t *p, f32x4_t v) {
+  const u32x2_t u = {static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16),
+                     static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16)};
+  *reinterpret_cast<u32x2_t *>(p) = u;
+}
+
 struct F2 {
   float a, b;
+};
+
+struct V2 {
+  f32x4_t a, b;
 };
 
 // Logits, transposed: C[v][n] = S[n][v] = Z[n] . W_out[v]  (rows = vocab ids,
@@ -161,61 +206,61 @@ struct EpiWeightGrad {
   }
 };
 
-// fp32 store with optional residual (Y = X + C) and accumulation (dW += C).
-// Rows at or beyond `rows` are not stored (the GEMM may run over padding).
+// fp32 store with optional accumulation (dW += C).  Rows at or beyond
+// `rows` are not stored (the GEMM may run over padding).
 template <typename T>
 struct EpiStoreF32 {
   struct Params {
     float *C;
     int64_t ldc;
-    const T *residual;  // same layout as C, or NULL
-    int64_t ldr;
     int rows;
     int accumulate;
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    with_flag(p.residual != nullptr, [&](auto R_) EE_ALWAYS_INLINE {
-      with_flag(p.accumulate != 0, [&](auto A_) EE_ALWAYS_INLINE {
-        constexpr bool kRes = decltype(R_)::value, kAcc = decltype(A_)::value;
-        if constexpr (!kRes && !kAcc) {
-          for_each_acc<Cfg>(acc, t, [&](int row, int col, int, float a) EE_ALWAYS_INLINE {
-            if (row < p.rows && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = a;
-          });
-        } else {
-          for_each_acc_loaded<Cfg>(
-              acc, t, p.rows, t.N,
-              [&](int row, int col) EE_ALWAYS_INLINE {
-                float r = 0.0f;
-                if constexpr (kRes) r += to_f32(p.residual[static_cast<int64_t>(row) * p.ldr + col]);
-                if constexpr (kAcc) r += p.C[static_cast<int64_t>(row) * p.ldc + col];
-                return r;
-              },
-              [&](int row, int col, int, float a, float in) EE_ALWAYS_INLINE {
-                if (row < p.rows && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = a + in;
-              });
-        }
-      });
+    with_flag(p.accumulate != 0, [&](auto A_) EE_ALWAYS_INLINE {
+      if constexpr (!decltype(A_)::value) {
+        for_each_acc<Cfg>(acc, t, [&](int row, int col, int, float a) EE_ALWAYS_INLINE {
+          if (row < p.rows && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = a;
+        });
+      } else {
+        for_each_acc_loaded<Cfg>(
+            acc, t, p.rows, t.N,
+            [&](int row, int col) EE_ALWAYS_INLINE { return p.C[static_cast<int64_t>(row) * p.ldc + col]; },
+            [&](int row, int col, int, float a, float in) EE_ALWAYS_INLINE {
+              if (row < p.rows && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = a + in;
+            });
+      }
     });
   }
 };
 
-// Store in the element type (gate projection H_g of the SwiGLU MLP).
+// The SwiGLU MLP's GEMMs run transposed: rows of C are features (I or h)
+// and columns are tokens, while every activation is stored token-major
+// ([N][I] or [N][h]), so each lane's four consecutive rows are one vector
+// access.  Feature counts are multiples of 64, so a group of four rows is
+// either wholly inside the problem or wholly outside.
+
+// Gate projection: H_g[n][i] = C[i][n], stored in the element type.
 template <typename T>
-struct EpiStoreT {
+struct EpiStoreTr {
   struct Params {
-    T *C;
+    T *C;          // [N][ldc]
     int64_t ldc;
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc<Cfg>(acc, t, [&](int row, int col, int, float a) EE_ALWAYS_INLINE {
-      if (row < t.M && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = from_f32<T>(a);
-    });
+    for_each_acc4_loaded<Cfg>(
+        acc, t, [&](int, int) EE_ALWAYS_INLINE { return 0; },
+        [&](int row0, int col, int, f32x4_t c, int) EE_ALWAYS_INLINE {
+          if (row0 < t.M && col < t.N) store4(p.C + static_cast<int64_t>(col) * p.ldc + row0, c);
+        });
   }
 };
 
-// Up projection H_u with the SwiGLU product: A = silu(H_g) * H_u.
+// Up projection with the SwiGLU product, untransposed (rows of C are
+// tokens): H_u = C, A = silu(H_g) * H_u.  Lanes 0-31 of each access cover 32
+// consecutive features of one token row.
 template <typename T>
 struct EpiSwiGLU {
   struct Params {
@@ -239,10 +284,57 @@ struct EpiSwiGLU {
   }
 };
 
-// Backward of the SwiGLU product from dA = dY W_down:
+// Up projection with the SwiGLU product: H_u[n][i] = C[i][n],
+// A[n][i] = silu(H_g[n][i]) * H_u[n][i].
+template <typename T>
+struct EpiSwiGLUTr {
+  struct Params {
+    const T *Hg;
+    T *Hu;
+    T *A;
+    int64_t ld;
+  };
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    for_each_acc4_loaded<Cfg>(
+        acc, t, [&](int row0, int col) EE_ALWAYS_INLINE { return load4(p.Hg + static_cast<int64_t>(col) * p.ld + row0); },
+        [&](int row0, int col, int, f32x4_t hu, f32x4_t hg) EE_ALWAYS_INLINE {
+          if (row0 < t.M && col < t.N) {
+            const int64_t o = static_cast<int64_t>(col) * p.ld + row0;
+            store4(p.Hu + o, hu);
+            f32x4_t a;
+            static_for<4>([&](auto e) EE_ALWAYS_INLINE {
+              constexpr int E = decltype(e)::value;
+              a[E] = silu_f(hg[E]) * hu[E];
+            });
+            store4(p.A + o, a);
+          }
+        });
+  }
+};
+
+// Down projection with the residual: Y[n][j] = X[n][j] + C[j][n]  (fp32 out).
+template <typename T>
+struct EpiResidualTr {
+  struct Params {
+    float *Y;       // [N][ld]
+    const T *X;     // [N][ld]
+    int64_t ld;
+  };
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    for_each_acc4_loaded<Cfg>(
+        acc, t, [&](int row0, int col) EE_ALWAYS_INLINE { return load4(p.X + static_cast<int64_t>(col) * p.ld + row0); },
+        [&](int row0, int col, int, f32x4_t c, f32x4_t x) EE_ALWAYS_INLINE {
+          if (row0 < t.M && col < t.N) store4(p.Y + static_cast<int64_t>(col) * p.ld + row0, c + x);
+        });
+  }
+};
+
+// Backward of the SwiGLU product from dA[n][i] = C[i][n] (C = W_down^T dY^T):
 //   dH_g = dA * H_u * silu'(H_g),   dH_u = dA * silu(H_g).
 template <typename T>
-struct EpiSwiGLUBwd {
+struct EpiSwiGLUBwdTr {
   struct Params {
     const T *Hg;
     const T *Hu;
@@ -252,17 +344,23 @@ struct EpiSwiGLUBwd {
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc_loaded<Cfg>(
-        acc, t, t.M, t.N,
-        [&](int row, int col) EE_ALWAYS_INLINE {
-          const int64_t o = static_cast<int64_t>(row) * p.ld + col;
-          return F2{to_f32(p.Hg[o]), to_f32(p.Hu[o])};
+    for_each_acc4_loaded<Cfg>(
+        acc, t,
+        [&](int row0, int col) EE_ALWAYS_INLINE {
+          const int64_t o = static_cast<int64_t>(col) * p.ld + row0;
+          return V2{load4(p.Hg + o), load4(p.Hu + o)};
         },
-        [&](int row, int col, int, float da, F2 h) EE_ALWAYS_INLINE {
-          if (row < t.M && col < t.N) {
-            const int64_t o = static_cast<int64_t>(row) * p.ld + col;
-            p.dHg[o] = from_f32<T>(da * h.b * silu_grad_f(h.a));
-            p.dHu[o] = from_f32<T>(da * silu_f(h.a));
+        [&](int row0, int col, int, f32x4_t da, V2 h) EE_ALWAYS_INLINE {
+          if (row0 < t.M && col < t.N) {
+            const int64_t o = static_cast<int64_t>(col) * p.ld + row0;
+            f32x4_t dg, du;
+            static_for<4>([&](auto e) EE_ALWAYS_INLINE {
+              constexpr int E = decltype(e)::value;
+              dg[E] = da[E] * h.b[E] * silu_grad_f(h.a[E]);
+              du[E] = da[E] * silu_f(h.a[E]);
+            });
+            store4(p.dHg + o, dg);
+            store4(p.dHu + o, du);
           }
         });
   }

@@ -429,9 +429,9 @@ hipError_t gemm_weight_grad_mn(bool f32, const void *g, const void *xhat, int m,
 hipError_t gemm_gate(bool f32, const void *u, const void *w_gate, int n, int inter, int h, void *hg,
                      hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiStoreT<T>::Params ep{static_cast<T *>(hg), inter};
-    return run_gemm<T, true, true, EpiStoreT<T>>(Operand{u, h}, Operand{w_gate, h}, GemmShape{n, inter, h},
-                                                    ep, stream);
+    typename EpiStoreTr<T>::Params ep{static_cast<T *>(hg), inter};
+    return run_gemm<T, true, true, EpiStoreTr<T>>(Operand{w_gate, h}, Operand{u, h}, GemmShape{inter, n, h},
+                                                     ep, stream);
   });
   return hipSuccess;
 }
@@ -450,9 +450,9 @@ hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int 
 hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, const void *x, int n, int h,
                               int inter, float *y, hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiStoreF32<T>::Params ep{y, h, static_cast<const T *>(x), h, n, 0};
-    return run_gemm<T, true, true, EpiStoreF32<T>>(Operand{act, inter}, Operand{w_down, inter},
-                                                      GemmShape{n, h, inter}, ep, stream);
+    typename EpiResidualTr<T>::Params ep{y, static_cast<const T *>(x), h};
+    return run_gemm<T, true, true, EpiResidualTr<T>>(Operand{w_down, inter}, Operand{act, inter},
+                                                        GemmShape{h, n, inter}, ep, stream);
   });
   return hipSuccess;
 }
@@ -460,7 +460,7 @@ hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, con
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab, float *dz,
                    hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiStoreF32<T>::Params ep{dz, h, nullptr, 0, n, 0};
+    typename EpiStoreF32<T>::Params ep{dz, h, n, 0};
     return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{g_t, ldn}, Operand{w_out, h},
                                                         GemmShape{ldn, h, vocab}, ep, stream);
   });
@@ -470,10 +470,10 @@ hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn,
 hipError_t gemm_da_swiglu(bool f32, const void *dy, const void *w_down, int n, int inter, int h, const void *hg,
                           const void *hu, void *dhg, void *dhu, hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiSwiGLUBwd<T>::Params ep{static_cast<const T *>(hg), static_cast<const T *>(hu),
-                                        static_cast<T *>(dhg), static_cast<T *>(dhu), inter};
-    return run_gemm<T, true, false, EpiSwiGLUBwd<T>>(Operand{dy, h}, Operand{w_down, inter},
-                                                        GemmShape{n, inter, h}, ep, stream);
+    typename EpiSwiGLUBwdTr<T>::Params ep{static_cast<const T *>(hg), static_cast<const T *>(hu),
+                                          static_cast<T *>(dhg), static_cast<T *>(dhu), inter};
+    return run_gemm<T, false, true, EpiSwiGLUBwdTr<T>>(Operand{w_down, inter}, Operand{dy, h},
+                                                          GemmShape{inter, n, h}, ep, stream);
   });
   return hipSuccess;
 }
@@ -481,7 +481,7 @@ hipError_t gemm_da_swiglu(bool f32, const void *dy, const void *w_down, int n, i
 hipError_t gemm_dw_down(bool f32, const void *dy, const void *act, int n, int h, int inter, float *dwd,
                         int accumulate, hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiStoreF32<T>::Params ep{dwd, inter, nullptr, 0, h, accumulate};
+    typename EpiStoreF32<T>::Params ep{dwd, inter, h, accumulate};
     return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{dy, h}, Operand{act, inter},
                                                         GemmShape{h, inter, n}, ep, stream);
   });

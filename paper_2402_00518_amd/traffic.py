@@ -39,10 +39,10 @@ LABEL_KERNELS = {
     "down gradient": ("false, false, ee::EpiStoreF32<", 1),
     "gate gradient": ("false, false, ee::EpiWeightGrad<", 0),
     "up gradient": ("false, false, ee::EpiWeightGrad<", 1),
-    "gate projection": ("ee::EpiStoreT<", None),
+    "gate projection": ("ee::EpiStoreTr<", None),
     "up projection + swiglu": ("ee::EpiSwiGLU<", None),
-    "down projection + residual": ("true, true, ee::EpiStoreF32<", None),
-    "dA + swiglu backward": ("ee::EpiSwiGLUBwd<", None),
+    "down projection + residual": ("ee::EpiResidualTr<", None),
+    "dA + swiglu backward": ("ee::EpiSwiGLUBwdTr<", None),
     "logit seed": ("seed_kernel", None),
     "cross-entropy reduce": ("ce_reduce_kernel", None),
 }
