@@ -75,6 +75,33 @@ def measured_traffic(workload, kernel):
     return rec.get("bytes_per_launch")
 
 
+def adam_leg(sess, steps, warmup):
+    """The Adam update of every exit parameter (fp32 master, bf16 parameter)
+    after the step: HBM-bound, 30 algorithmic bytes per parameter (read g, m,
+    v, master; write m, v, master and the bf16 copy; 28 for fp32 without a
+    master)."""
+    import torch
+    sess.init_optimizer(master=True)
+    for t in range(1, warmup + 1):
+        sess.update(t, 1e-4)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for t in range(warmup + 1, warmup + steps + 1):
+        sess.update(t, 1e-4)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    n_params, n_bytes = 0, 0
+    for params in sess.params:
+        for p in params.values():
+            n_params += p.numel()
+            n_bytes += p.numel() * (30 if p.dtype == torch.bfloat16 else 28)
+    gbps = n_bytes / (ms / 1e3) / 1e9
+    return {"ms": ms, "params": n_params, "bytes_per_launch": n_bytes, "achieved_GBps": gbps,
+            "peak_GBps": PEAK_HBM_GBS, "frac": gbps / PEAK_HBM_GBS, "bound": "hbm"}
+
+
 def copy_calibration(mib, copies=3):
     """Plain device-to-device copies of a known size; a counter run over the
     bench reads them to calibrate FETCH_SIZE and WRITE_SIZE."""
@@ -126,6 +153,8 @@ def main():
                     help="tokens of the batch the oracle runs on (0: all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-pass", action="store_true")
+    ap.add_argument("--no-update-leg", action="store_true",
+                    help="skip timing the Adam update of the exit parameters")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the step, copy a buffer of this size 3 times (counter calibration)")
     args = ap.parse_args()
@@ -212,6 +241,11 @@ def main():
                                "traffic": measured_traffic(w.name, dom),
                                "flops_per_launch": f, "avg_ms": kernels[dom]["avg_ms"]}
         log(f"dominant kernel {dom}: {kernels[dom]['avg_ms']:.4f} ms")
+
+    if not args.no_update_leg:
+        out["adam_update"] = adam_leg(sess, args.steps, args.warmup)
+        a = out["adam_update"]
+        log(f"adam update: {a['ms']:.4f} ms, {a['achieved_GBps']:.0f} GB/s ({100 * a['frac']:.1f}% of HBM peak)")
 
     if args.copy_calibration_mib > 0:
         copy_calibration(args.copy_calibration_mib)

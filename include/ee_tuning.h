@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define EE_ABI_VERSION 1
+#define EE_ABI_VERSION 2
 
 typedef enum ee_status {
   EE_OK = 0,
@@ -178,10 +178,60 @@ ee_status ee_multi_exit_step(int n_exits, const ee_exit *exits,
  * clears the record.  EE_OK otherwise. */
 ee_status ee_check_device_error(void *ws, size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------- update
+ * Adam update of exit parameters: the optimiser of Sec. 4 ("Tuning": Adam
+ * with beta1 = 0.9, beta2 = 0.95, eps = 1e-5), the last part of a tuning
+ * iteration (Sec. 3.2, "Computational efficiency").  For every element, in
+ * fp32, with t = step:
+ *
+ *   m <- beta1 m + (1 - beta1) g
+ *   v <- beta2 v + (1 - beta2) g^2
+ *   p <- p - lr * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ *
+ * (Kingma and Ba's update; no weight decay, no clipping: the paper names
+ * neither).  p is the fp32 master copy when `master` is given, and the
+ * stored parameter then receives p rounded to its dtype (bf16: to nearest
+ * even); without a master the stored parameter is read, updated and written
+ * back.  One call updates any number of tensors (fused, up to 8 per kernel
+ * launch). */
+typedef struct ee_adam_tensor {
+  void *param;         /* device [numel] of `dtype`, updated in place            */
+  float *master;       /* device fp32 [numel] master weights, or NULL            */
+  const float *grad;   /* device fp32 [numel], e.g. from ee_head_backward        */
+  float *exp_avg;      /* device fp32 [numel] first moment m (zeros before t=1)  */
+  float *exp_avg_sq;   /* device fp32 [numel] second moment v (zeros before t=1) */
+  int64_t numel;       /* >= 0; 0 skips the tensor (its pointers may be NULL)    */
+  int32_t dtype;       /* ee_dtype of param                                      */
+  int32_t reserved;    /* must be 0                                              */
+} ee_adam_tensor;
+
+/* tensors: host array of n_tensors descriptors (n_tensors >= 0).
+ * lr: this update's step size (finite, e.g. from ee_lr_schedule); beta1,
+ * beta2 in [0, 1); eps >= 0; step >= 1 counts this update.
+ * Errors (nothing is enqueued): EE_ERR_NULL for a missing pointer of a
+ * non-empty tensor, EE_ERR_ALIGN, EE_ERR_DTYPE, EE_ERR_SHAPE (numel < 0, a
+ * reserved field set, hyper-parameters out of range), EE_ERR_ALIAS when a
+ * written buffer (param, master, exp_avg, exp_avg_sq of any tensor)
+ * overlaps another buffer of the call. */
+ee_status ee_adam_update(int n_tensors, const ee_adam_tensor *tensors, float lr,
+                         float beta1, float beta2, float eps, int64_t step,
+                         void *stream);
+
+/* Learning rate of update `step` (1-based) under the schedule of Sec. 4
+ * ("Tuning": linear warmup over a fraction of the iterations, then linear
+ * decay from lr_max to lr_min).  With W = floor(warmup_fraction *
+ * total_steps):  lr_max * step / W for step <= W;  lr_min + (lr_max - lr_min)
+ * (total_steps - step) / (total_steps - W) up to total_steps;  lr_min after.
+ * Host function.  Returns NaN (and sets ee_last_error) if step < 1,
+ * total_steps < 1 or warmup_fraction is outside [0, 1). */
+double ee_lr_schedule(int64_t step, int64_t total_steps, double warmup_fraction,
+                      double lr_max, double lr_min);
+
 /* Kernel timing, for diagnostics.  Between ee_profile_start() and
- * ee_profile_stop(), every kernel the step functions launch is bracketed by a
- * pair of HIP events recorded on the launch stream (the events cost a few
- * microseconds per launch; keep them out of headline timings).
+ * ee_profile_stop(), every kernel the step and update functions launch is
+ * bracketed by a pair of HIP events recorded on the launch stream (the
+ * events cost a few microseconds per launch; keep them out of headline
+ * timings).
  * ee_profile_stop() waits for the recorded events, fills up to `capacity`
  * entries of `out` (host array) with per-kernel launch counts and summed
  * durations, in first-launch order, and returns the number of entries, or -1

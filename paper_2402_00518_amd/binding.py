@@ -35,13 +35,14 @@ EE_EXIT_LAYER = 3
 
 EE_FLAG_DYNAMIC_TOKEN_WEIGHTS = 1
 
-EE_ABI_VERSION = 1
+EE_ABI_VERSION = 2
 
 # Every symbol include/ee_tuning.h declares.
 EXPORTS = (
     "ee_workspace_bytes", "ee_head_forward_loss", "ee_head_backward",
     "ee_multi_exit_step", "ee_check_device_error", "ee_status_string",
     "ee_last_error", "ee_abi_version", "ee_profile_start", "ee_profile_stop",
+    "ee_adam_update", "ee_lr_schedule",
 )
 
 
@@ -62,6 +63,14 @@ class EeExitGrads(ctypes.Structure):
         ("d_w_out", ctypes.c_void_p), ("d_gamma", ctypes.c_void_p),
         ("d_gamma_mlp", ctypes.c_void_p), ("d_w_gate", ctypes.c_void_p),
         ("d_w_up", ctypes.c_void_p), ("d_w_down", ctypes.c_void_p),
+    ]
+
+
+class EeAdamTensor(ctypes.Structure):
+    _fields_ = [
+        ("param", ctypes.c_void_p), ("master", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+        ("exp_avg", ctypes.c_void_p), ("exp_avg_sq", ctypes.c_void_p),
+        ("numel", ctypes.c_int64), ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32),
     ]
 
 
@@ -114,6 +123,10 @@ def lib() -> ctypes.CDLL:
         L.ee_profile_start.restype = i32
         L.ee_profile_stop.argtypes = [P(EeKernelTime), i32]
         L.ee_profile_stop.restype = i32
+        L.ee_adam_update.argtypes = [i32, P(EeAdamTensor), f32, f32, f32, f32, i64, vp]
+        L.ee_adam_update.restype = i32
+        L.ee_lr_schedule.argtypes = [i64, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double]
+        L.ee_lr_schedule.restype = ctypes.c_double
         _lib = L
     return _lib
 
@@ -224,3 +237,28 @@ def make_grads(d_w_out=None, d_gamma=None, d_gamma_mlp=None, d_w_gate=None, d_w_
                d_w_down=None) -> EeExitGrads:
     return EeExitGrads(ptr(d_w_out), ptr(d_gamma), ptr(d_gamma_mlp), ptr(d_w_gate), ptr(d_w_up),
                        ptr(d_w_down))
+
+
+def adam_tensor(param, grad, exp_avg, exp_avg_sq, master=None, numel: Optional[int] = None,
+                dtype: Optional[int] = None) -> EeAdamTensor:
+    """Descriptor of one parameter tensor for ee_adam_update.  With torch
+    tensors, numel and dtype default to the parameter's."""
+    if numel is None:
+        numel = param.numel()
+    if dtype is None:
+        import torch
+        dtype = EE_BF16 if param.dtype == torch.bfloat16 else EE_F32
+    return EeAdamTensor(ptr(param), ptr(master), ptr(grad), ptr(exp_avg), ptr(exp_avg_sq),
+                        int(numel), int(dtype), 0)
+
+
+def ee_adam_update(tensors: Sequence[EeAdamTensor], lr: float, beta1: float, beta2: float,
+                   eps: float, step: int, stream, check=True) -> int:
+    arr = (EeAdamTensor * max(1, len(tensors)))(*tensors)
+    s = lib().ee_adam_update(len(tensors), arr, lr, beta1, beta2, eps, step, stream)
+    return _check(s, "ee_adam_update") if check else s
+
+
+def ee_lr_schedule(step: int, total_steps: int, warmup_fraction: float, lr_max: float,
+                   lr_min: float) -> float:
+    return lib().ee_lr_schedule(step, total_steps, warmup_fraction, lr_max, lr_min)

@@ -505,6 +505,95 @@ ee_status ee_multi_exit_step(int n_exits, const ee_exit *exits, const void *cons
   return EE_OK;
 }
 
+ee_status ee_adam_update(int n_tensors, const ee_adam_tensor *tensors, float lr, float beta1, float beta2,
+                         float eps, int64_t step, void *stream) {
+  if (n_tensors < 0) return fail(EE_ERR_SHAPE, "n_tensors = %d is negative", n_tensors);
+  if (n_tensors == 0) return EE_OK;
+  if (tensors == nullptr) return fail(EE_ERR_NULL, "tensors is NULL");
+  if (!std::isfinite(lr)) return fail(EE_ERR_SHAPE, "lr is not finite");
+  if (!(beta1 >= 0.0f && beta1 < 1.0f) || !(beta2 >= 0.0f && beta2 < 1.0f))
+    return fail(EE_ERR_SHAPE, "beta1 = %g and beta2 = %g must lie in [0, 1)", beta1, beta2);
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return fail(EE_ERR_SHAPE, "eps = %g must be finite and >= 0", eps);
+  if (step < 1) return fail(EE_ERR_SHAPE, "step = %lld must be >= 1", static_cast<long long>(step));
+  std::vector<Range> written, read;
+  for (int i = 0; i < n_tensors; ++i) {
+    const ee_adam_tensor &t = tensors[i];
+    if (t.reserved != 0) return fail(EE_ERR_SHAPE, "tensor %d: reserved field must be 0", i);
+    if (t.numel < 0) return fail(EE_ERR_SHAPE, "tensor %d: numel is negative", i);
+    if (t.dtype != EE_F32 && t.dtype != EE_BF16) return fail(EE_ERR_DTYPE, "tensor %d: unknown dtype %d", i, t.dtype);
+    if (t.numel == 0) continue;
+    if (t.numel > (int64_t{1} << 40)) return fail(EE_ERR_SHAPE, "tensor %d: numel above 2^40", i);
+    char what[64];
+    snprintf(what, sizeof(what), "tensor %d param", i);
+    EE_TRY(check_ptr(t.param, what));
+    snprintf(what, sizeof(what), "tensor %d grad", i);
+    EE_TRY(check_ptr(t.grad, what));
+    snprintf(what, sizeof(what), "tensor %d exp_avg", i);
+    EE_TRY(check_ptr(t.exp_avg, what));
+    snprintf(what, sizeof(what), "tensor %d exp_avg_sq", i);
+    EE_TRY(check_ptr(t.exp_avg_sq, what));
+    snprintf(what, sizeof(what), "tensor %d master", i);
+    EE_TRY(check_opt_ptr(t.master, what));
+    const size_t n = static_cast<size_t>(t.numel);
+    written.push_back(make_range(t.param, n * (t.dtype == EE_BF16 ? 2 : 4), "a param"));
+    written.push_back(make_range(t.exp_avg, n * 4, "an exp_avg"));
+    written.push_back(make_range(t.exp_avg_sq, n * 4, "an exp_avg_sq"));
+    if (t.master != nullptr) written.push_back(make_range(t.master, n * 4, "a master"));
+    read.push_back(make_range(t.grad, n * 4, "a grad"));
+  }
+  for (size_t a = 0; a < written.size(); ++a) {
+    for (size_t b = a + 1; b < written.size(); ++b)
+      if (overlap(written[a], written[b]))
+        return fail(EE_ERR_ALIAS, "%s buffer overlaps %s buffer", written[a].what, written[b].what);
+    for (const Range &r : read)
+      if (overlap(written[a], r)) return fail(EE_ERR_ALIAS, "%s buffer overlaps %s buffer", written[a].what, r.what);
+  }
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  ee::AdamBatchArgs b{};
+  b.beta1 = beta1;
+  b.beta2 = beta2;
+  b.eps = eps;
+  const double t = static_cast<double>(step);
+  b.lr_bc1 = static_cast<float>(static_cast<double>(lr) / (1.0 - std::pow(static_cast<double>(beta1), t)));
+  b.inv_bc2 = static_cast<float>(1.0 / (1.0 - std::pow(static_cast<double>(beta2), t)));
+  int64_t blocks = 0;
+  for (int i = 0; i < n_tensors; ++i) {
+    const ee_adam_tensor &t = tensors[i];
+    if (t.numel == 0) continue;
+    const int64_t nb = ee::adam_blocks(t.numel);
+    if (b.count == ee::kAdamMaxTensors || blocks + nb > 0x7FFFFFFF) {
+      EE_LAUNCH("adam update", s, ee::launch_adam(b, s));
+      b.count = 0;
+      blocks = 0;
+    }
+    ee::AdamTensorArgs &a = b.t[b.count++];
+    a = ee::AdamTensorArgs{};
+    a.param = t.param;
+    a.master = t.master;
+    a.grad = t.grad;
+    a.exp_avg = t.exp_avg;
+    a.exp_avg_sq = t.exp_avg_sq;
+    a.numel = t.numel;
+    a.bf16 = t.dtype == EE_BF16;
+    blocks += nb;
+  }
+  if (b.count > 0) EE_LAUNCH("adam update", s, ee::launch_adam(b, s));
+  return EE_OK;
+}
+
+double ee_lr_schedule(int64_t step, int64_t total_steps, double warmup_fraction, double lr_max, double lr_min) {
+  if (step < 1 || total_steps < 1 || !(warmup_fraction >= 0.0 && warmup_fraction < 1.0)) {
+    fail(EE_ERR_SHAPE, "ee_lr_schedule: need step >= 1, total_steps >= 1, 0 <= warmup_fraction < 1");
+    return std::nan("");
+  }
+  const int64_t warmup = static_cast<int64_t>(std::floor(warmup_fraction * static_cast<double>(total_steps)));
+  if (step <= warmup) return lr_max * static_cast<double>(step) / static_cast<double>(warmup);
+  if (step <= total_steps)
+    return lr_min + (lr_max - lr_min) * static_cast<double>(total_steps - step) /
+                        static_cast<double>(total_steps - warmup);
+  return lr_min;
+}
+
 ee_status ee_profile_start(void) {
   std::lock_guard<std::mutex> g(g_prof_mu);
   g_prof_records.clear();

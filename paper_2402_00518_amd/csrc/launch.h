@@ -97,4 +97,30 @@ hipError_t gemm_da_swiglu(bool f32, const void *dy, const void *w_down, int n, i
 hipError_t gemm_dw_down(bool f32, const void *dy, const void *act, int n, int h, int inter, float *dwd,
                         int accumulate, hipStream_t stream);
 
+// ------------------------------------------------------------- optimizer
+// One tensor of a fused Adam launch (optim.hip).  Pointers are device
+// addresses, 16-byte aligned; master may be NULL.
+constexpr int kAdamMaxTensors = 8;
+struct AdamTensorArgs {
+  void *param;            // [numel], bf16 when `bf16`, else fp32
+  float *master;          // [numel] or NULL
+  const float *grad;      // [numel]
+  float *exp_avg;         // [numel]
+  float *exp_avg_sq;      // [numel]
+  int64_t numel;
+  int64_t first_block;    // set by launch_adam
+  int32_t bf16;
+  int32_t pad;
+};
+struct AdamBatchArgs {
+  AdamTensorArgs t[kAdamMaxTensors];
+  int32_t count;
+  float beta1, beta2, eps;
+  float lr_bc1;           // lr / (1 - beta1^step)
+  float inv_bc2;          // 1 / (1 - beta2^step)
+};
+// Blocks one tensor of `numel` elements occupies in a launch.
+int64_t adam_blocks(int64_t numel);
+hipError_t launch_adam(AdamBatchArgs b, hipStream_t stream);
+
 }  // namespace ee

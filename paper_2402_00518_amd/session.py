@@ -76,6 +76,7 @@ class Session:
         self.loss_total = torch.zeros(1, dtype=torch.float32, device=self.device)
         self.loss_per_exit = torch.zeros(max(ne, 1), dtype=torch.float32, device=self.device)
         self.row_loss = torch.zeros(self.n_tokens, dtype=torch.float32, device=self.device)
+        self.opt_state: Optional[List[dict]] = None
 
     @classmethod
     def from_batch(cls, batch, device: str = "cuda:0") -> "Session":
@@ -110,3 +111,34 @@ class Session:
 
     def check_device_error(self):
         B.ee_check_device_error(self.ws, self.ws_bytes, current_stream())
+
+    # ------------------------------------------------------------ optimizer
+    def init_optimizer(self, master: bool = True):
+        """Adam state for every exit parameter: zero moments and, with
+        `master`, an fp32 master copy of each parameter."""
+        self.opt_state = []
+        for params in self.params:
+            st = {}
+            for name, p in params.items():
+                st[name] = {
+                    "m": torch.zeros(p.shape, dtype=torch.float32, device=self.device),
+                    "v": torch.zeros(p.shape, dtype=torch.float32, device=self.device),
+                    "master": p.float().clone() if master else None,
+                }
+            self.opt_state.append(st)
+
+    def adam_tensors(self) -> List[B.EeAdamTensor]:
+        out = []
+        for params, grads, st in zip(self.params, self.grads, self.opt_state):
+            for name, p in params.items():
+                s = st[name]
+                out.append(B.adam_tensor(p, grads["d_" + name], s["m"], s["v"], master=s["master"]))
+        return out
+
+    def update(self, step: int, lr: float, beta1: float = 0.9, beta2: float = 0.95, eps: float = 1e-5,
+               stream: Optional[int] = None):
+        """One ee_adam_update over every exit parameter (Sec. 4 hyper-parameters by default)."""
+        if self.opt_state is None:
+            self.init_optimizer()
+        B.ee_adam_update(self.adam_tensors(), lr, beta1, beta2, eps, step,
+                         current_stream() if stream is None else stream)

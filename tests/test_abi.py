@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_version_and_status_strings():
-    assert B.ee_abi_version() == B.EE_ABI_VERSION == 1
+    assert B.ee_abi_version() == B.EE_ABI_VERSION == 2
     for s in range(10):
         assert B.ee_status_string(s)
     assert "unknown" in B.ee_status_string(99)
@@ -211,3 +211,73 @@ def test_missing_library_fails_loudly(tmp_path, monkeypatch):
     monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "libeetune.so"))
     with pytest.raises(RuntimeError, match="missing"):
         B.lib()
+
+
+# ------------------------------------------------------------ Adam update
+def fake_adam(i=0, numel=1000, dtype=B.EE_BF16, master=True):
+    base = 0x40_0000_0000 + i * 8 * GB
+    return B.adam_tensor(param=base, grad=base + GB, exp_avg=base + 2 * GB, exp_avg_sq=base + 3 * GB,
+                         master=(base + 4 * GB) if master else None, numel=numel, dtype=dtype)
+
+
+def adam_status(tensors, lr=1e-4, b1=0.9, b2=0.95, eps=1e-5, step=1):
+    return B.ee_adam_update(tensors, lr, b1, b2, eps, step, None, check=False)
+
+
+def test_adam_nothing_to_do_is_ok():
+    assert adam_status([]) == B.EE_OK
+    assert adam_status([fake_adam(numel=0), fake_adam(1, numel=0)]) == B.EE_OK
+
+
+@pytest.mark.parametrize("kw,code,needle", [
+    (dict(lr=float("nan")), B.EE_ERR_SHAPE, "lr"),
+    (dict(b1=1.0), B.EE_ERR_SHAPE, "beta1"),
+    (dict(b2=-0.1), B.EE_ERR_SHAPE, "beta1"),
+    (dict(eps=-1.0), B.EE_ERR_SHAPE, "eps"),
+    (dict(step=0), B.EE_ERR_SHAPE, "step"),
+])
+def test_adam_rejects_bad_hyperparameters(kw, code, needle):
+    assert adam_status([fake_adam()], **kw) == code
+    assert needle in B.ee_last_error()
+
+
+def test_adam_rejects_bad_tensors():
+    t = fake_adam(); t.param = None
+    assert adam_status([t]) == B.EE_ERR_NULL and "param" in B.ee_last_error()
+    t = fake_adam(); t.grad = 0x40_0000_0008
+    assert adam_status([t]) == B.EE_ERR_ALIGN and "grad" in B.ee_last_error()
+    t = fake_adam(); t.master = 0x40_0000_0004
+    assert adam_status([t]) == B.EE_ERR_ALIGN
+    t = fake_adam(); t.dtype = 7
+    assert adam_status([t]) == B.EE_ERR_DTYPE
+    t = fake_adam(); t.numel = -1
+    assert adam_status([t]) == B.EE_ERR_SHAPE
+    t = fake_adam(); t.reserved = 1
+    assert adam_status([t]) == B.EE_ERR_SHAPE
+
+
+def test_adam_rejects_aliasing():
+    t = fake_adam(); t.exp_avg_sq = t.exp_avg + 512       # m and v overlap
+    assert adam_status([t]) == B.EE_ERR_ALIAS
+    t = fake_adam(); t.grad = t.param                     # written param over the gradient
+    assert adam_status([t]) == B.EE_ERR_ALIAS
+    a, b = fake_adam(0), fake_adam(1)
+    b.master = a.master + 16                              # two tensors share a master
+    assert adam_status([a, b]) == B.EE_ERR_ALIAS
+    a, b = fake_adam(0), fake_adam(1)
+    b.grad = a.grad                                        # shared read-only gradient is fine for validation
+    b.param = a.param + 1024                               # but overlapping params (2000 bytes each) are not
+    assert adam_status([a, b]) == B.EE_ERR_ALIAS
+
+
+def test_lr_schedule_matches_the_oracle():
+    from oracle import optim as OP
+    for T, f, hi, lo in ((40000, 0.01, 1e-4, 1e-5), (10, 0.0, 1.0, 0.0), (37, 0.3, 2.0, 0.5)):
+        for s in sorted({1, 2, int(f * T), int(f * T) + 1, T // 2, T - 1, T, T + 3}):
+            if s < 1:
+                continue
+            assert B.ee_lr_schedule(s, T, f, hi, lo) == pytest.approx(OP.lr_schedule(s, T, f, hi, lo),
+                                                                      rel=1e-15, abs=1e-300)
+    import math
+    assert math.isnan(B.ee_lr_schedule(0, 10, 0.1, 1.0, 0.0))
+    assert math.isnan(B.ee_lr_schedule(1, 10, 1.0, 1.0, 0.0))
