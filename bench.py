@@ -102,6 +102,51 @@ def adam_leg(sess, steps, warmup):
             "peak_GBps": PEAK_HBM_GBS, "frac": gbps / PEAK_HBM_GBS, "bound": "hbm"}
 
 
+def decode_leg(sess, rows_list=(1, 8, 32), iters=50):
+    """The confidence-based exit decision of exit 0 at decode (forward only,
+    a few rows): HBM-bound, algorithmic bytes = every exit weight read once
+    plus the rows' hidden states.  Reports the whole call and, from the
+    library's kernel timer, the output-matrix kernel alone."""
+    import torch
+    from paper_2402_00518_amd import binding as B
+    e = sess.c_exits[0]
+    es = 2 if sess.dtype == B.EE_BF16 else 4
+    w_bytes = sum(p.numel() * p.element_size() for p in sess.params[0].values())
+    w_out_bytes = sess.params[0]["w_out"].numel() * es
+    out = {}
+    for rows in rows_list:
+        x = sess.x[0][:rows]
+        ws_bytes = B.ee_decode_workspace_bytes(e, rows)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+        tok = torch.empty(rows, dtype=torch.int32, device="cuda")
+        conf = torch.empty(rows, dtype=torch.float32, device="cuda")
+        flag = torch.empty(rows, dtype=torch.int32, device="cuda")
+        stream = torch.cuda.current_stream().cuda_stream
+        call = lambda: B.ee_exit_decide(e, x, rows, 0.9, tok, conf, flag, ws, ws_bytes, stream)
+        for _ in range(5):
+            call()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(iters):
+            call()
+        b.record()
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) / iters * 1e3
+        B.ee_profile_start()
+        for _ in range(iters):
+            call()
+        kt = B.ee_profile_stop()
+        n, t = kt["decode logits partials"]
+        k_us = t / n * 1e3
+        total = w_bytes + rows * sess.hidden * es
+        out[str(rows)] = {"us": us, "achieved_GBps": total / (us / 1e6) / 1e9,
+                          "logits_kernel_us": k_us,
+                          "logits_kernel_GBps": w_out_bytes / (k_us / 1e6) / 1e9,
+                          "frac": (w_out_bytes / (k_us / 1e6) / 1e9) / PEAK_HBM_GBS}
+    return {"bound": "hbm", "peak_GBps": PEAK_HBM_GBS, "threshold": 0.9, "rows": out}
+
+
 def copy_calibration(mib, copies=3):
     """Plain device-to-device copies of a known size; a counter run over the
     bench reads them to calibrate FETCH_SIZE and WRITE_SIZE."""
@@ -154,7 +199,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-pass", action="store_true")
     ap.add_argument("--no-update-leg", action="store_true",
-                    help="skip timing the Adam update of the exit parameters")
+                    help="skip timing the Adam update and the decode-time exit decision")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the step, copy a buffer of this size 3 times (counter calibration)")
     args = ap.parse_args()
@@ -246,6 +291,12 @@ def main():
         out["adam_update"] = adam_leg(sess, args.steps, args.warmup)
         a = out["adam_update"]
         log(f"adam update: {a['ms']:.4f} ms, {a['achieved_GBps']:.0f} GB/s ({100 * a['frac']:.1f}% of HBM peak)")
+
+    if not args.no_update_leg:
+        out["exit_decision"] = decode_leg(sess)
+        for r, d in out["exit_decision"]["rows"].items():
+            log(f"exit decision rows={r}: {d['us']:.1f} us per call, output-matrix kernel {d['logits_kernel_us']:.1f} us "
+                f"({d['logits_kernel_GBps']:.0f} GB/s, {100 * d['frac']:.1f}% of HBM peak)")
 
     if args.copy_calibration_mib > 0:
         copy_calibration(args.copy_calibration_mib)

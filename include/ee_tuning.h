@@ -178,6 +178,32 @@ ee_status ee_multi_exit_step(int n_exits, const ee_exit *exits,
  * clears the record.  EE_OK otherwise. */
 ee_status ee_check_device_error(void *ws, size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------- decode
+ * Confidence-based exit decision at decode time (Sec. 4, "Inference":
+ * greedy decoding; an exit emits its most likely token as soon as the
+ * maximum next-token probability there is above a threshold, and a
+ * threshold of 1 disables early exits).  Forward only, for n_rows hidden
+ * states at one exit (typically the batch of sequences being decoded):
+ *
+ *   S_n          = exit(hidden_n) W_out^T          (the architectures above)
+ *   token[n]     = argmax_v S_n[v], the lowest id among tied maxima
+ *   confidence[n]= max_v softmax(S_n)[v]           (fp32)
+ *   exit_flag[n] = confidence[n] > threshold ? 1 : 0   ("above": strict)
+ *
+ *   hidden      device [n_rows][h], dtype of the exit.
+ *   token, exit_flag  device int32 [n_rows];  confidence device fp32 [n_rows].
+ *   ws          device workspace of ws_bytes >= ee_decode_workspace_bytes().
+ * Errors as for the training entry points (nothing is enqueued); threshold
+ * must not be NaN.  Logits are accumulated in fp32 from the exit's dtype;
+ * no logit tensor is written (each 32-row slice of W_out is reduced to
+ * per-token max / argmax / sum of exponentials on the fly). */
+size_t ee_decode_workspace_bytes(const ee_exit *e, int64_t n_rows);
+
+ee_status ee_exit_decide(const ee_exit *e, const void *hidden, int64_t n_rows,
+                         float threshold, int32_t *token, float *confidence,
+                         int32_t *exit_flag, void *ws, size_t ws_bytes,
+                         void *stream);
+
 /* ---------------------------------------------------------------- update
  * Adam update of exit parameters: the optimiser of Sec. 4 ("Tuning": Adam
  * with beta1 = 0.9, beta2 = 0.95, eps = 1e-5), the last part of a tuning

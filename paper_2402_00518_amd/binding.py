@@ -42,7 +42,7 @@ EXPORTS = (
     "ee_workspace_bytes", "ee_head_forward_loss", "ee_head_backward",
     "ee_multi_exit_step", "ee_check_device_error", "ee_status_string",
     "ee_last_error", "ee_abi_version", "ee_profile_start", "ee_profile_stop",
-    "ee_adam_update", "ee_lr_schedule",
+    "ee_adam_update", "ee_lr_schedule", "ee_decode_workspace_bytes", "ee_exit_decide",
 )
 
 
@@ -127,6 +127,10 @@ def lib() -> ctypes.CDLL:
         L.ee_adam_update.restype = i32
         L.ee_lr_schedule.argtypes = [i64, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double]
         L.ee_lr_schedule.restype = ctypes.c_double
+        L.ee_decode_workspace_bytes.argtypes = [P(EeExit), i64]
+        L.ee_decode_workspace_bytes.restype = ctypes.c_size_t
+        L.ee_exit_decide.argtypes = [P(EeExit), vp, i64, f32, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.ee_exit_decide.restype = i32
         _lib = L
     return _lib
 
@@ -262,3 +266,17 @@ def ee_adam_update(tensors: Sequence[EeAdamTensor], lr: float, beta1: float, bet
 def ee_lr_schedule(step: int, total_steps: int, warmup_fraction: float, lr_max: float,
                    lr_min: float) -> float:
     return lib().ee_lr_schedule(step, total_steps, warmup_fraction, lr_max, lr_min)
+
+
+def ee_decode_workspace_bytes(e: EeExit, n_rows: int) -> int:
+    n = lib().ee_decode_workspace_bytes(ctypes.byref(e), n_rows)
+    if n == 0:
+        raise EEError(EE_ERR_SHAPE, "ee_decode_workspace_bytes", ee_last_error())
+    return n
+
+
+def ee_exit_decide(e: EeExit, hidden, n_rows: int, threshold: float, token, confidence, exit_flag,
+                   ws, ws_bytes: int, stream, check=True) -> int:
+    s = lib().ee_exit_decide(ctypes.byref(e), ptr(hidden), n_rows, threshold, ptr(token),
+                             ptr(confidence), ptr(exit_flag), ptr(ws), ws_bytes, stream)
+    return _check(s, "ee_exit_decide") if check else s

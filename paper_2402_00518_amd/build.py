@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libeetune.so")
 
-SOURCES = ["kernels.hip", "optim.hip", "ee_abi.cpp"]
+SOURCES = ["kernels.hip", "optim.hip", "decode.hip", "ee_abi.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

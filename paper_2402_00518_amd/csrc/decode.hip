@@ -1,0 +1,346 @@
+// Decode-time exit head (Sec. 4 "Inference": greedy decoding with a
+// confidence-based exit): a handful of rows through one exit, forward only.
+//
+// At decode the products are skinny, C[r][j] = sum_k W[r][k] Z[j][k] with
+// a weight W of R rows and only B <= 32 token rows Z per pass, so they are
+// bound by streaming W from HBM once.  One wave owns 32 rows of W and reads
+// them straight into MFMA A fragments (16 bytes of K per lane), 16
+// fragments in flight per lane per group of K, with no LDS; the token rows
+// come from L2 as B fragments (tokens past B re-read row B-1 and their
+// outputs are dropped).  bf16 uses v_mfma_f32_32x32x16_bf16, fp32
+// v_mfma_f32_32x32x2_f32 over the same 16-byte loads.
+//
+// Epilogues: store (gate projection), SwiGLU (up projection), residual
+// (down projection) and, for the output matrix, per-wave softmax partials:
+// for each token the maximum logit over the wave's rows, the lowest row
+// reaching it and sum exp(S - max).  decide_kernel combines the partials
+// of all waves into the greedy token, its probability and the exit flag.
+#include <hip/hip_runtime.h>
+
+#include "ee_device.h"
+#include "launch.h"
+
+namespace ee {
+
+namespace {
+
+constexpr int kDecRows = 32;    // rows of W per wave (one block of 64 threads)
+constexpr int kDecTokens = 32;  // token rows per pass (grid.y walks more)
+constexpr int kDecGroup = 16;   // fragment loads per lane in flight
+
+template <typename T> struct DecFrag;
+// bf16: a 16-byte load holds 8 values of K; one MFMA consumes 16 (two lane halves).
+template <> struct DecFrag<bf16_t> {
+  static constexpr int K_PER_LOAD = 16;  // values of K covered by one load across the wave
+  __device__ __forceinline__ static void mma(const u32x4_t &a, const u32x4_t &b, f32x16_t &acc) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                  acc, 0, 0, 0);
+  }
+};
+// fp32: a 16-byte load holds 4 values of K; four MFMAs of K = 2 (lane halves
+// hold K offsets 0-3 and 4-7 of the same 8, in the same order for A and B).
+template <> struct DecFrag<float> {
+  static constexpr int K_PER_LOAD = 8;
+  __device__ __forceinline__ static void mma(const u32x4_t &a, const u32x4_t &b, f32x16_t &acc) {
+    static_for<4>([&](auto e) EE_ALWAYS_INLINE {
+      constexpr int E = decltype(e)::value;
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[E]), __uint_as_float(b[E]), acc, 0, 0, 0);
+    });
+  }
+};
+
+// acc[v] of lane l: row r0 + (v/4)*8 + (l/32)*4 + v%4, token j0 + l%32.
+__device__ __forceinline__ int dec_row(int r0, int lane, int v) {
+  return r0 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+}
+
+template <typename T, class Epi>
+__global__ __launch_bounds__(64) void skinny_kernel(const T *__restrict__ W, int64_t ldw, int R,
+                                                    const T *__restrict__ Z, int64_t ldz, int B, int K,
+                                                    typename Epi::Params ep) {
+  constexpr int KL = DecFrag<T>::K_PER_LOAD;
+  constexpr int PER_LOAD = 16 / sizeof(T);  // elements of one 16-byte load
+  const int lane = threadIdx.x;
+  const int r0 = blockIdx.x * kDecRows, j0 = blockIdx.y * kDecTokens;
+  const int wr = min(r0 + (lane & 31), R - 1);
+  const int zr = min(j0 + (lane & 31), B - 1);
+  const int koff = (lane >> 5) * PER_LOAD;
+  const char *wp = reinterpret_cast<const char *>(W + static_cast<int64_t>(wr) * ldw + koff);
+  const char *zp = reinterpret_cast<const char *>(Z + static_cast<int64_t>(zr) * ldz + koff);
+  f32x16_t acc;
+  static_for<16>([&](auto v) EE_ALWAYS_INLINE { acc[decltype(v)::value] = 0.0f; });
+
+  // Groups of kDecGroup loads (K multiple of the group's K), then groups of 4.
+  constexpr int KG = kDecGroup * KL;
+  int k = 0;
+  for (; k + KG <= K; k += KG) {
+    u32x4_t a[kDecGroup], b[kDecGroup];
+    static_for<kDecGroup>([&](auto q) EE_ALWAYS_INLINE {
+      constexpr int Q = decltype(q)::value;
+      a[Q] = *reinterpret_cast<const u32x4_t *>(wp + (static_cast<int64_t>(k) + Q * KL) * sizeof(T));
+      b[Q] = *reinterpret_cast<const u32x4_t *>(zp + (static_cast<int64_t>(k) + Q * KL) * sizeof(T));
+    });
+    // Keep every load of the group ahead of the MFMAs: left alone, the
+    // scheduler would trade loads in flight for registers.
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<kDecGroup>([&](auto q) EE_ALWAYS_INLINE { DecFrag<T>::mma(a[decltype(q)::value], b[decltype(q)::value], acc); });
+  }
+  constexpr int KG4 = 4 * KL;
+  for (; k < K; k += KG4) {
+    u32x4_t a[4], b[4];
+    static_for<4>([&](auto q) EE_ALWAYS_INLINE {
+      constexpr int Q = decltype(q)::value;
+      a[Q] = *reinterpret_cast<const u32x4_t *>(wp + (static_cast<int64_t>(k) + Q * KL) * sizeof(T));
+      b[Q] = *reinterpret_cast<const u32x4_t *>(zp + (static_cast<int64_t>(k) + Q * KL) * sizeof(T));
+    });
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<4>([&](auto q) EE_ALWAYS_INLINE { DecFrag<T>::mma(a[decltype(q)::value], b[decltype(q)::value], acc); });
+  }
+  Epi::apply(ep, acc, r0, j0, lane, R, B);
+}
+
+// Four consecutive rows of one token as fp32 (bf16 or fp32 storage).
+template <typename T> __device__ __forceinline__ f32x4_t dload4(const T *p);
+template <> __device__ __forceinline__ f32x4_t dload4<float>(const float *p) {
+  return *reinterpret_cast<const f32x4_t *>(p);
+}
+template <> __device__ __forceinline__ f32x4_t dload4<bf16_t>(const bf16_t *p) {
+  const u32x2_t u = *reinterpret_cast<const u32x2_t *>(p);
+  return f32x4_t{__uint_as_float(u[0] << 16), __uint_as_float(u[0] & 0xFFFF0000u), __uint_as_float(u[1] << 16),
+                 __uint_as_float(u[1] & 0xFFFF0000u)};
+}
+template <typename T> __device__ __forceinline__ void dstore4(T *p, f32x4_t v);
+template <> __device__ __forceinline__ void dstore4<float>(float *p, f32x4_t v) {
+  *reinterpret_cast<f32x4_t *>(p) = v;
+}
+template <> __device__ __forceinline__ void dstore4<bf16_t>(bf16_t *p, f32x4_t v) {
+  const u32x2_t u = {static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16),
+                     static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16)};
+  *reinterpret_cast<u32x2_t *>(p) = u;
+}
+
+// f(row0, token, vals) for each group of 4 consecutive rows of the lane
+// (rows are feature indices, a multiple of 4 apart from the tile origin;
+// R is a multiple of 64 for the MLP products that use this).
+template <class F>
+__device__ __forceinline__ void for_rows4(const f32x16_t &acc, int r0, int j0, int lane, int R, int B, F &&f) {
+  const int j = j0 + (lane & 31);
+  if (j >= B) return;
+  static_for<4>([&](auto q) EE_ALWAYS_INLINE {
+    constexpr int Q = decltype(q)::value;
+    const int row0 = dec_row(r0, lane, 4 * Q);
+    if (row0 < R) f(row0, j, f32x4_t{acc[4 * Q], acc[4 * Q + 1], acc[4 * Q + 2], acc[4 * Q + 3]});
+  });
+}
+
+template <typename T>
+struct DecStore {  // out[j][r] = C[r][j]
+  struct Params {
+    T *out;
+    int64_t ld;
+  };
+  __device__ __forceinline__ static void apply(const Params &p, const f32x16_t &acc, int r0, int j0, int lane, int R,
+                                               int B) {
+    for_rows4(acc, r0, j0, lane, R, B, [&](int row0, int j, f32x4_t c) EE_ALWAYS_INLINE {
+      dstore4<T>(p.out + static_cast<int64_t>(j) * p.ld + row0, c);
+    });
+  }
+};
+
+template <typename T>
+struct DecSwiGLU {  // A[j][r] = silu(Hg[j][r]) * C[r][j]
+  struct Params {
+    const T *hg;
+    T *act;
+    int64_t ld;
+  };
+  __device__ __forceinline__ static void apply(const Params &p, const f32x16_t &acc, int r0, int j0, int lane, int R,
+                                               int B) {
+    for_rows4(acc, r0, j0, lane, R, B, [&](int row0, int j, f32x4_t hu) EE_ALWAYS_INLINE {
+      const int64_t o = static_cast<int64_t>(j) * p.ld + row0;
+      const f32x4_t hg = dload4<T>(p.hg + o);
+      f32x4_t a;
+      static_for<4>([&](auto e) EE_ALWAYS_INLINE {
+        constexpr int E = decltype(e)::value;
+        a[E] = silu_f(hg[E]) * hu[E];
+      });
+      dstore4<T>(p.act + o, a);
+    });
+  }
+};
+
+template <typename T>
+struct DecResidual {  // Y[j][r] = X[j][r] + C[r][j]  (fp32 out)
+  struct Params {
+    const T *x;
+    float *y;
+    int64_t ld;
+  };
+  __device__ __forceinline__ static void apply(const Params &p, const f32x16_t &acc, int r0, int j0, int lane, int R,
+                                               int B) {
+    for_rows4(acc, r0, j0, lane, R, B, [&](int row0, int j, f32x4_t c) EE_ALWAYS_INLINE {
+      const int64_t o = static_cast<int64_t>(j) * p.ld + row0;
+      dstore4<float>(p.y + o, c + dload4<T>(p.x + o));
+    });
+  }
+};
+
+// Softmax partials of the output-matrix product over the wave's 32 rows
+// (vocabulary ids), per token: m = max, arg = lowest id reaching m,
+// l = sum exp(S - m).  Stored at [wave tile][token].
+struct DecLogits {
+  struct Params {
+    float *part_m;
+    float *part_l;
+    int32_t *part_arg;
+    int ld;  // tokens per partial row (B)
+  };
+  __device__ __forceinline__ static void apply(const Params &p, const f32x16_t &acc, int r0, int j0, int lane, int R,
+                                               int B) {
+    float m = -INFINITY;
+    int arg = r0;  // a valid id even if no logit compares (NaN)
+    static_for<16>([&](auto v) EE_ALWAYS_INLINE {
+      constexpr int Vv = decltype(v)::value;
+      const int row = dec_row(r0, lane, Vv);
+      const float s = acc[Vv];
+      if (row < R && (s > m || (s == m && row < arg))) {
+        m = s;
+        arg = row;
+      }
+    });
+    const float om = __shfl_xor(m, 32);
+    const int oa = __shfl_xor(arg, 32);
+    if (om > m || (om == m && oa < arg)) {
+      m = om;
+      arg = oa;
+    }
+    float l = 0.0f;
+    static_for<16>([&](auto v) EE_ALWAYS_INLINE {
+      constexpr int Vv = decltype(v)::value;
+      if (dec_row(r0, lane, Vv) < R) l += __expf(acc[Vv] - m);
+    });
+    l += __shfl_xor(l, 32);
+    const int j = j0 + lane;
+    if (lane < 32 && j < B) {
+      const int64_t o = static_cast<int64_t>(blockIdx.x) * p.ld + j;
+      p.part_m[o] = m;
+      p.part_l[o] = l;
+      p.part_arg[o] = arg;
+    }
+  }
+};
+
+// One block of 256 threads per token: combine the tiles' partials.
+__global__ __launch_bounds__(256) void decide_kernel(const float *part_m, const float *part_l,
+                                                     const int32_t *part_arg, int tiles, int B, float threshold,
+                                                     int32_t *token, float *confidence, int32_t *exit_flag) {
+  __shared__ float sm[256];
+  __shared__ int st[256];
+  __shared__ float sl[256];
+  const int j = blockIdx.x, tid = threadIdx.x;
+  // max over tiles, and the lowest tile reaching it (its arg is the lowest id)
+  // t_best < 0: no tile seen.  The first tile a thread sees is always taken,
+  // so the result is a valid tile even when no maximum compares (NaN).
+  float m = -INFINITY;
+  int t_best = -1;
+  for (int t = tid; t < tiles; t += 256) {
+    const float v = part_m[static_cast<int64_t>(t) * B + j];
+    if (t_best < 0 || v > m) {  // t increases, so the first tile reaching the maximum is kept
+      m = v;
+      t_best = t;
+    }
+  }
+  sm[tid] = m;
+  st[tid] = t_best;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) {
+      const float om = sm[tid + s];
+      const int ot = st[tid + s];
+      if (ot >= 0 && (st[tid] < 0 || om > sm[tid] || (om == sm[tid] && ot < st[tid]))) {
+        sm[tid] = om;
+        st[tid] = ot;
+      }
+    }
+    __syncthreads();
+  }
+  const float mx = sm[0];
+  const int tb = st[0];
+  float l = 0.0f;
+  for (int t = tid; t < tiles; t += 256) {
+    const int64_t o = static_cast<int64_t>(t) * B + j;
+    l += part_l[o] * __expf(part_m[o] - mx);
+  }
+  sl[tid] = l;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) sl[tid] += sl[tid + s];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const float conf = 1.0f / sl[0];
+    token[j] = part_arg[static_cast<int64_t>(tb) * B + j];
+    confidence[j] = conf;
+    exit_flag[j] = conf > threshold ? 1 : 0;
+  }
+}
+
+template <typename T, class Epi>
+hipError_t launch_skinny(const void *W, int64_t ldw, int R, const void *Z, int64_t ldz, int B, int K,
+                         const typename Epi::Params &ep, hipStream_t stream) {
+  if (R <= 0 || B <= 0) return hipSuccess;
+  if (K % (4 * DecFrag<T>::K_PER_LOAD) != 0) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>((R + kDecRows - 1) / kDecRows),
+                  static_cast<unsigned>((B + kDecTokens - 1) / kDecTokens));
+  hipLaunchKernelGGL((skinny_kernel<T, Epi>), grid, dim3(64), 0, stream, static_cast<const T *>(W), ldw, R,
+                     static_cast<const T *>(Z), ldz, B, K, ep);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int decode_tiles(int rows) { return (rows + kDecRows - 1) / kDecRows; }
+
+hipError_t decode_store(bool f32, const void *w, int rows, const void *z, int n, int k, void *out,
+                        hipStream_t stream) {
+  if (f32)
+    return launch_skinny<float, DecStore<float>>(w, k, rows, z, k, n, k, {static_cast<float *>(out), rows}, stream);
+  return launch_skinny<bf16_t, DecStore<bf16_t>>(w, k, rows, z, k, n, k, {static_cast<bf16_t *>(out), rows},
+                                                 stream);
+}
+
+hipError_t decode_swiglu(bool f32, const void *w, int rows, const void *z, int n, int k, const void *hg,
+                         void *act, hipStream_t stream) {
+  if (f32)
+    return launch_skinny<float, DecSwiGLU<float>>(
+        w, k, rows, z, k, n, k, {static_cast<const float *>(hg), static_cast<float *>(act), rows}, stream);
+  return launch_skinny<bf16_t, DecSwiGLU<bf16_t>>(
+      w, k, rows, z, k, n, k, {static_cast<const bf16_t *>(hg), static_cast<bf16_t *>(act), rows}, stream);
+}
+
+hipError_t decode_residual(bool f32, const void *w, int rows, const void *z, int n, int k, const void *x,
+                           float *y, hipStream_t stream) {
+  if (f32)
+    return launch_skinny<float, DecResidual<float>>(w, k, rows, z, k, n, k,
+                                                    {static_cast<const float *>(x), y, rows}, stream);
+  return launch_skinny<bf16_t, DecResidual<bf16_t>>(w, k, rows, z, k, n, k,
+                                                    {static_cast<const bf16_t *>(x), y, rows}, stream);
+}
+
+hipError_t decode_logits(bool f32, const void *w_out, int vocab, const void *z, int n, int h, float *part_m,
+                         float *part_l, int32_t *part_arg, hipStream_t stream) {
+  const DecLogits::Params ep{part_m, part_l, part_arg, n};
+  if (f32) return launch_skinny<float, DecLogits>(w_out, h, vocab, z, h, n, h, ep, stream);
+  return launch_skinny<bf16_t, DecLogits>(w_out, h, vocab, z, h, n, h, ep, stream);
+}
+
+hipError_t decode_decide(const float *part_m, const float *part_l, const int32_t *part_arg, int tiles, int n,
+                         float threshold, int32_t *token, float *confidence, int32_t *exit_flag,
+                         hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(decide_kernel, dim3(static_cast<unsigned>(n)), dim3(256), 0, stream, part_m, part_l, part_arg,
+                     tiles, n, threshold, token, confidence, exit_flag);
+  return hipGetLastError();
+}
+
+}  // namespace ee

@@ -386,6 +386,85 @@ ee_status check_aliasing(int n_exits, const ee_exit *exits, const void *const *h
   return EE_OK;
 }
 
+// ------------------------------------------------------------ decode
+// Workspace regions of the decode-time decision for n rows.
+struct DecLayout {
+  size_t z = 0, r = 0, u = 0, rx = 0, hg = 0, act = 0, y = 0, pm = 0, pl = 0, pa = 0, total = 0;
+  int tiles = 0;
+};
+
+DecLayout dec_layout(const ee_exit &e, int64_t n) {
+  DecLayout L;
+  const size_t es = e.dtype == EE_BF16 ? 2 : 4;
+  const size_t h = static_cast<size_t>(e.hidden), I = static_cast<size_t>(e.intermediate);
+  const size_t N = static_cast<size_t>(n);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.z = take(N * h * es);
+  L.r = take(N * 4);
+  if (e.kind == EE_EXIT_MLP) {
+    L.u = take(N * h * es);
+    L.rx = take(N * 4);
+    L.hg = take(N * I * es);
+    L.act = take(N * I * es);
+    L.y = take(N * h * 4);
+  }
+  L.tiles = ee::decode_tiles(static_cast<int>(e.vocab));
+  L.pm = take(static_cast<size_t>(L.tiles) * N * 4);
+  L.pl = take(static_cast<size_t>(L.tiles) * N * 4);
+  L.pa = take(static_cast<size_t>(L.tiles) * N * 4);
+  L.total = off;
+  return L;
+}
+
+ee_status validate_rows(int64_t n) {
+  if (n < 1 || n > kMaxTokens)
+    return fail(EE_ERR_SHAPE, "n_rows=%lld must be in [1, %lld]", static_cast<long long>(n),
+                static_cast<long long>(kMaxTokens));
+  return EE_OK;
+}
+
+ee_status run_decide(const ee_exit &e, const void *x, int64_t n64, float threshold, int32_t *token,
+                     float *confidence, int32_t *exit_flag, void *ws, hipStream_t s) {
+  const DecLayout L = dec_layout(e, n64);
+  const bool f32 = e.dtype == EE_F32;
+  const int n = static_cast<int>(n64), h = static_cast<int>(e.hidden), V = static_cast<int>(e.vocab);
+  const int I = static_cast<int>(e.intermediate);
+  const void *z = x;
+  if (e.kind == EE_EXIT_MLP) {
+    EE_LAUNCH("decode mlp pre-norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.rx), s));
+    EE_LAUNCH("decode mlp pre-norm apply", s,
+              ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.rx), e.gamma_mlp, n, n, h, at(ws, L.u), nullptr,
+                                    nullptr, s));
+    EE_LAUNCH("decode gate projection", s, ee::decode_store(f32, e.w_gate, I, at(ws, L.u), n, h, at(ws, L.hg), s));
+    EE_LAUNCH("decode up projection + swiglu", s,
+              ee::decode_swiglu(f32, e.w_up, I, at(ws, L.u), n, h, at(ws, L.hg), at(ws, L.act), s));
+    EE_LAUNCH("decode down projection + residual", s,
+              ee::decode_residual(f32, e.w_down, h, at(ws, L.act), n, I, x, atf(ws, L.y), s));
+    EE_LAUNCH("decode exit norm rms", s, ee::launch_row_rms(true, atf(ws, L.y), h, n, h, e.rms_eps, atf(ws, L.r), s));
+    EE_LAUNCH("decode exit norm apply", s,
+              ee::launch_norm_apply(true, f32, atf(ws, L.y), h, atf(ws, L.r), e.gamma, n, n, h, at(ws, L.z), nullptr,
+                                    nullptr, s));
+    z = at(ws, L.z);
+  } else if (e.kind == EE_EXIT_NORM) {
+    EE_LAUNCH("decode exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s));
+    EE_LAUNCH("decode exit norm apply", s,
+              ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.r), e.gamma, n, n, h, at(ws, L.z), nullptr, nullptr, s));
+    z = at(ws, L.z);
+  }
+  int32_t *pa = reinterpret_cast<int32_t *>(at(ws, L.pa));
+  EE_LAUNCH("decode logits partials", s,
+            ee::decode_logits(f32, e.w_out, V, z, n, h, atf(ws, L.pm), atf(ws, L.pl), pa, s));
+  EE_LAUNCH("decode decision", s,
+            ee::decode_decide(atf(ws, L.pm), atf(ws, L.pl), pa, L.tiles, n, threshold, token, confidence, exit_flag,
+                              s));
+  return EE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -592,6 +671,40 @@ double ee_lr_schedule(int64_t step, int64_t total_steps, double warmup_fraction,
     return lr_min + (lr_max - lr_min) * static_cast<double>(total_steps - step) /
                         static_cast<double>(total_steps - warmup);
   return lr_min;
+}
+
+size_t ee_decode_workspace_bytes(const ee_exit *e, int64_t n_rows) {
+  g_last_error.clear();
+  if (validate_exit(e, 0) != EE_OK || validate_rows(n_rows) != EE_OK) return 0;
+  return dec_layout(*e, n_rows).total;
+}
+
+ee_status ee_exit_decide(const ee_exit *e, const void *hidden, int64_t n_rows, float threshold, int32_t *token,
+                         float *confidence, int32_t *exit_flag, void *ws, size_t ws_bytes, void *stream) {
+  g_last_error.clear();
+  EE_TRY(validate_exit(e, 0));
+  EE_TRY(validate_rows(n_rows));
+  if (std::isnan(threshold)) return fail(EE_ERR_SHAPE, "threshold is NaN");
+  EE_TRY(check_ptr(hidden, "hidden"));
+  EE_TRY(check_ptr(token, "token"));
+  EE_TRY(check_ptr(confidence, "confidence"));
+  EE_TRY(check_ptr(exit_flag, "exit_flag"));
+  EE_TRY(check_workspace(ws, ws_bytes, dec_layout(*e, n_rows).total));
+  const size_t n = static_cast<size_t>(n_rows);
+  const size_t es = e->dtype == EE_BF16 ? 2 : 4;
+  Range outs[4] = {make_range(token, n * 4, "token"), make_range(confidence, n * 4, "confidence"),
+                   make_range(exit_flag, n * 4, "exit_flag"), make_range(ws, ws_bytes, "workspace")};
+  Range ins[7];
+  int k = param_ranges(*e, ins);
+  ins[k++] = make_range(hidden, n * static_cast<size_t>(e->hidden) * es, "hidden");
+  for (int a = 0; a < 4; ++a) {
+    for (int b = a + 1; b < 4; ++b)
+      if (overlap(outs[a], outs[b])) return fail(EE_ERR_ALIAS, "%s overlaps %s", outs[a].what, outs[b].what);
+    for (int b = 0; b < k; ++b)
+      if (overlap(outs[a], ins[b])) return fail(EE_ERR_ALIAS, "%s overlaps %s", outs[a].what, ins[b].what);
+  }
+  return run_decide(*e, hidden, n_rows, threshold, token, confidence, exit_flag, ws,
+                    static_cast<hipStream_t>(stream));
 }
 
 ee_status ee_profile_start(void) {

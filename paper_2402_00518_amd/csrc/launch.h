@@ -119,6 +119,25 @@ struct AdamBatchArgs {
   float lr_bc1;           // lr / (1 - beta1^step)
   float inv_bc2;          // 1 / (1 - beta2^step)
 };
+// ---------------------------------------------------------------- decode
+// Skinny products of the decode-time exit head (decode.hip): n token rows
+// (any n; 32 per pass) against a weight of `rows` K-contiguous rows, K a
+// multiple of 64.  Outputs are token-major, [n][rows].
+int decode_tiles(int rows);  // partial rows per token of decode_logits
+hipError_t decode_store(bool f32, const void *w, int rows, const void *z, int n, int k, void *out,
+                        hipStream_t stream);
+hipError_t decode_swiglu(bool f32, const void *w, int rows, const void *z, int n, int k, const void *hg,
+                         void *act, hipStream_t stream);
+hipError_t decode_residual(bool f32, const void *w, int rows, const void *z, int n, int k, const void *x,
+                           float *y, hipStream_t stream);
+// Softmax partials of S = Z W_out^T: [decode_tiles(vocab)][n] max, sum exp, lowest argmax.
+hipError_t decode_logits(bool f32, const void *w_out, int vocab, const void *z, int n, int h, float *part_m,
+                         float *part_l, int32_t *part_arg, hipStream_t stream);
+// Greedy token, its probability, and confidence > threshold, per token row.
+hipError_t decode_decide(const float *part_m, const float *part_l, const int32_t *part_arg, int tiles, int n,
+                         float threshold, int32_t *token, float *confidence, int32_t *exit_flag,
+                         hipStream_t stream);
+
 // Blocks one tensor of `numel` elements occupies in a launch.
 int64_t adam_blocks(int64_t numel);
 hipError_t launch_adam(AdamBatchArgs b, hipStream_t stream);

@@ -281,3 +281,33 @@ def test_lr_schedule_matches_the_oracle():
     import math
     assert math.isnan(B.ee_lr_schedule(0, 10, 0.1, 1.0, 0.0))
     assert math.isnan(B.ee_lr_schedule(1, 10, 1.0, 1.0, 0.0))
+
+
+# ------------------------------------------------------------ decode decision
+def decide_status(e, n=4, threshold=0.5, token=0x50_0000_0000, conf=0x51_0000_0000, flag=0x52_0000_0000,
+                  ws=0x60_0000_0000, ws_bytes=1 << 32, hidden=X):
+    return B.ee_exit_decide(e, hidden, n, threshold, token, conf, flag, ws, ws_bytes, None, check=False)
+
+
+def test_decode_workspace_bytes():
+    e = fake_exit()
+    a, b = B.ee_decode_workspace_bytes(e, 1), B.ee_decode_workspace_bytes(e, 64)
+    assert 0 < a < b
+    m = fake_exit(kind=B.EE_EXIT_MLP, I=128)
+    assert B.ee_decode_workspace_bytes(m, 8) > B.ee_decode_workspace_bytes(fake_exit(), 8)
+    with pytest.raises(B.EEError):
+        B.ee_decode_workspace_bytes(e, 0)
+
+
+def test_decide_rejects_bad_arguments():
+    e = fake_exit()
+    assert decide_status(e, n=0) == B.EE_ERR_SHAPE
+    assert decide_status(e, threshold=float("nan")) == B.EE_ERR_SHAPE
+    assert decide_status(e, token=None) == B.EE_ERR_NULL
+    assert decide_status(e, conf=0x51_0000_0004) == B.EE_ERR_ALIGN
+    assert decide_status(e, ws_bytes=16) == B.EE_ERR_WORKSPACE
+    assert decide_status(e, flag=0x50_0000_0000) == B.EE_ERR_ALIAS          # flag over token
+    assert decide_status(e, token=X) == B.EE_ERR_ALIAS                       # output over the hidden states
+    assert decide_status(e, ws=0x10_0000_0000) == B.EE_ERR_ALIAS             # workspace over W_out
+    bad = fake_exit(); bad.kind = B.EE_EXIT_LAYER
+    assert decide_status(bad) == B.EE_ERR_UNSUPPORTED
