@@ -6,9 +6,9 @@ package.  The product path never does.
 
 from .ee_oracle import (  # noqa: F401
     EXIT_EMBEDDING, EXIT_MLP, EXIT_NORM, Exit, ExitResult, confidence,
-    exit_backward, exit_forward, exit_step, exit_step_sampled, log_sum_exp,
-    logit_grad, multi_exit_step, rms_inv, rmsnorm_backward, sigmoid, silu,
-    silu_grad, softmax, token_nll,
+    exit_backward, exit_forward, exit_step, exit_step_sampled, layer_stats,
+    layernorm_backward, log_sum_exp, logit_grad, multi_exit_step, norm_forward,
+    rms_inv, rmsnorm_backward, sigmoid, silu, silu_grad, softmax, token_nll,
 )
 
 
@@ -22,5 +22,6 @@ def exits_from_batch(batch):
         out.append(Exit(kind=p.kind, w_out=dec(p.w_out), gamma=dec(p.gamma),
                         gamma_mlp=dec(p.gamma_mlp), w_gate=dec(p.w_gate),
                         w_up=dec(p.w_up), w_down=dec(p.w_down),
-                        eps=batch.workload.eps))
+                        eps=batch.workload.eps, norm=batch.workload.norm,
+                        beta=dec(getattr(p, "beta", None))))
     return out

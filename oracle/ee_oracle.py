@@ -29,7 +29,11 @@ Readings where the paper is silent (each also listed in the design notes):
   R4 MLP exit: Y = X + W_d^T-projection of SwiGLU(RMSNorm_mlp(X)), then the
      exit RMSNorm and W_out, two separate gains;
   R5 SwiGLU: A = silu(U W_g^T) * (U W_u^T), silu(t) = t sigmoid(t), no biases;
-  R6 W_out is stored [V][h] (the paper's h x V matrix, transposed storage).
+  R6 W_out is stored [V][h] (the paper's h x V matrix, transposed storage);
+  R19 LayerNorm flavour (Sec. 3.1 names LayerNorm or RMSNorm): s_hat =
+     (s - mean_j s_j) (mean_j (s_j - mean)^2 + eps)^(-1/2) (biased variance,
+     eps inside the root), z = s_hat * gamma + beta with an optional bias;
+     an exit uses one normalisation type for all its norms.
 
 Every array here is float64; inputs are decoded exactly from their storage
 format before use.  Backward uses the plain chain rule (dZ = G W_out etc.),
@@ -78,6 +82,34 @@ def rms_inv(s: np.ndarray, eps: float) -> np.ndarray:
     return 1.0 / np.sqrt(np.mean(s * s, axis=1) + eps)
 
 
+def layer_stats(s: np.ndarray, eps: float):
+    """LayerNorm row statistics: mean and r = (mean_j (s_j - mean)^2 + eps)^(-1/2)
+    (biased variance, eps inside the root)."""
+    mu = np.mean(s, axis=1)
+    c = s - mu[:, None]
+    return mu, 1.0 / np.sqrt(np.mean(c * c, axis=1) + eps)
+
+
+def norm_forward(e: "Exit", s: np.ndarray, gain: np.ndarray, bias: Optional[np.ndarray]):
+    """The exit's normalisation of rows s: (s_hat, r, z) with z = s_hat * gain (+ bias)."""
+    if e.norm == "layer":
+        mu, r = layer_stats(s, e.eps)
+        s_hat = (s - mu[:, None]) * r[:, None]
+    else:
+        r = rms_inv(s, e.eps)
+        s_hat = s * r[:, None]
+    z = s_hat * gain[None, :]
+    if bias is not None:
+        z = z + bias[None, :]
+    return s_hat, r, z
+
+
+def layernorm_backward(d_hat: np.ndarray, s_hat: np.ndarray, r: np.ndarray) -> np.ndarray:
+    """ds for s_hat = (s - mean(s)) r:  r (d_hat - mean_j d_hat - s_hat mean_j(d_hat s_hat))."""
+    return r[:, None] * (d_hat - np.mean(d_hat, axis=1, keepdims=True)
+                         - s_hat * np.mean(d_hat * s_hat, axis=1, keepdims=True))
+
+
 def rmsnorm_backward(d_hat: np.ndarray, s_hat: np.ndarray, r: np.ndarray) -> np.ndarray:
     """Gradient w.r.t. the RMSNorm input s, given dL/d(s_hat) with s_hat = r s.
 
@@ -100,6 +132,8 @@ class Exit:
     w_up: Optional[np.ndarray] = None       # [I][h]
     w_down: Optional[np.ndarray] = None     # [h][I]
     eps: float = 1e-5
+    norm: str = "rms"                       # "rms" or "layer" (Sec. 3.1: LayerNorm or RMSNorm)
+    beta: Optional[np.ndarray] = None       # [h]  LayerNorm bias of the exit norm, or None
 
     @property
     def hidden(self) -> int:
@@ -113,6 +147,8 @@ class Exit:
         names = ["w_out"]
         if self.kind in (EXIT_NORM, EXIT_MLP):
             names.append("gamma")
+        if self.kind in (EXIT_NORM, EXIT_MLP) and self.beta is not None:
+            names.append("beta")
         if self.kind == EXIT_MLP:
             names += ["gamma_mlp", "w_gate", "w_up", "w_down"]
         return names
@@ -126,9 +162,7 @@ def exit_forward(e: Exit, x: np.ndarray) -> Dict[str, np.ndarray]:
     """
     f: Dict[str, np.ndarray] = {"x": x}
     if e.kind == EXIT_MLP:
-        r_x = rms_inv(x, e.eps)                      # pre-norm (Fig. 2 caption)
-        u_hat = x * r_x[:, None]
-        u = u_hat * e.gamma_mlp[None, :]
+        u_hat, r_x, u = norm_forward(e, x, e.gamma_mlp, None)   # pre-norm (Fig. 2 caption)
         hg = u @ e.w_gate.T                          # gate projection
         hu = u @ e.w_up.T                            # up projection
         a = silu(hg) * hu                            # SwiGLU (R5)
@@ -138,9 +172,7 @@ def exit_forward(e: Exit, x: np.ndarray) -> Dict[str, np.ndarray]:
     else:
         s_in = x
     if e.kind in (EXIT_NORM, EXIT_MLP):
-        r = rms_inv(s_in, e.eps)                     # exit Norm (Sec. 3.1, 4.2)
-        z_hat = s_in * r[:, None]
-        z = z_hat * e.gamma[None, :]
+        z_hat, r, z = norm_forward(e, s_in, e.gamma, e.beta)     # exit Norm (Sec. 3.1, 4.2)
         f.update(r=r, z_hat=z_hat)
     else:
         z = s_in                                     # Embedding exit
@@ -182,10 +214,13 @@ def exit_backward(e: Exit, f: Dict[str, np.ndarray], g: np.ndarray) -> Dict[str,
         return grads
     dz = g @ e.w_out                                 # dL/dZ      [n][h]
     grads["gamma"] = np.sum(dz * f["z_hat"], axis=0)
+    if e.beta is not None:
+        grads["beta"] = np.sum(dz, axis=0)
     if e.kind == EXIT_NORM:
         return grads
     d_zhat = dz * e.gamma[None, :]
-    dy = rmsnorm_backward(d_zhat, f["z_hat"], f["r"])  # through the exit norm
+    norm_bwd = layernorm_backward if e.norm == "layer" else rmsnorm_backward
+    dy = norm_bwd(d_zhat, f["z_hat"], f["r"])        # through the exit norm
     # y = x + a W_d^T: the residual branch carries no parameters.
     grads["w_down"] = dy.T @ f["a"]                  # [h][I]
     da = dy @ e.w_down                               # [n][I]
@@ -311,10 +346,13 @@ def exit_step_sampled(e: Exit, x: np.ndarray, y: np.ndarray, exit_weight: float,
             continue
         dz = g @ e.w_out
         add("gamma", np.sum(dz * f["z_hat"], axis=0))
+        if e.beta is not None:
+            add("beta", np.sum(dz, axis=0))
         if e.kind == EXIT_NORM:
             continue
         d_zhat = dz * e.gamma[None, :]
-        dy = rmsnorm_backward(d_zhat, f["z_hat"], f["r"])
+        norm_bwd = layernorm_backward if e.norm == "layer" else rmsnorm_backward
+        dy = norm_bwd(d_zhat, f["z_hat"], f["r"])
         da = dy @ e.w_down
         d_hg = da * f["hu"] * silu_grad(f["hg"])
         d_hu = da * silu(f["hg"])

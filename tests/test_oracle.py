@@ -409,3 +409,98 @@ def test_tiny_workload_loss_near_expectation():
     r = O.exit_step(e, W.decode(b.hidden[0]), b.targets)
     expect = math.log(1024) + 0.02 ** 2 * 256 / 2
     assert abs(r.loss - expect) < 0.1
+
+
+# ------------------------------------------------ LayerNorm flavour of Norm
+def rand_layer_exit(kind, h, V, I, rng, bias=True, eps=1e-5):
+    e = rand_exit(kind, h, V, I, rng, eps=eps)
+    e.norm = "layer"
+    if bias:
+        e.beta = 0.3 * rng.standard_normal(h)
+    return e
+
+
+@pytest.mark.parametrize("kind,bias", [(O.EXIT_NORM, True), (O.EXIT_NORM, False), (O.EXIT_MLP, True)])
+def test_layernorm_against_torch_autograd(kind, bias):
+    rng = np.random.default_rng(70 + kind + 2 * bias)
+    N, h, V, I, eps = 6, 16, 21, 20, 1e-5
+    e = rand_layer_exit(kind, h, V, I, rng, bias=bias, eps=eps)
+    x = rng.standard_normal((N, h)) + rng.standard_normal((N, 1)) * 2.0   # rows with offsets
+    y = rng.integers(0, V, N)
+    w = 0.6
+    r = O.exit_step(e, x, y, w)
+    tp = {k: torch.tensor(getattr(e, k), requires_grad=True) for k in e.param_names()}
+    tx = torch.tensor(x)
+    if kind == O.EXIT_MLP:
+        u = F.layer_norm(tx, (h,), tp["gamma_mlp"], None, eps)
+        a = F.silu(F.linear(u, tp["w_gate"])) * F.linear(u, tp["w_up"])
+        s_in = tx + F.linear(a, tp["w_down"])
+    else:
+        s_in = tx
+    z = F.layer_norm(s_in, (h,), tp["gamma"], tp.get("beta"), eps)
+    loss = F.cross_entropy(F.linear(z, tp["w_out"]), torch.tensor(y), reduction="mean")
+    (w * loss).backward()
+    assert r.loss == pytest.approx(loss.item(), rel=1e-13)
+    assert set(r.grads) == set(tp)
+    for k in e.param_names():
+        np.testing.assert_allclose(r.grads[k], tp[k].grad.numpy(), rtol=1e-10, atol=1e-14)
+
+
+def test_layernorm_finite_differences():
+    rng = np.random.default_rng(80)
+    N, h, V = 5, 8, 13
+    e = rand_layer_exit(O.EXIT_NORM, h, V, 0, rng)
+    x = rng.standard_normal((N, h)) + 1.5
+    y = rng.integers(0, V, N)
+    r = O.exit_step(e, x, y, 0.7)
+    for name in ("beta", "gamma"):
+        p = getattr(e, name)
+        for j in range(h):
+            old = p[j]
+            p[j] = old + 1e-6
+            lp = loss_only(e, x, y, 0.7)
+            p[j] = old - 1e-6
+            lm = loss_only(e, x, y, 0.7)
+            p[j] = old
+            assert (lp - lm) / 2e-6 == pytest.approx(r.grads[name][j], rel=1e-6, abs=1e-10)
+
+
+def test_layernorm_ignores_row_offsets_rmsnorm_does_not():
+    rng = np.random.default_rng(81)
+    N, h, V = 4, 12, 9
+    x = rng.standard_normal((N, h))
+    shift = rng.standard_normal((N, 1)) * 3.0
+    y = rng.integers(0, V, N)
+    e = rand_layer_exit(O.EXIT_NORM, h, V, 0, rng)
+    assert O.exit_step(e, x + shift, y).loss == pytest.approx(O.exit_step(e, x, y).loss, rel=1e-9)
+    e.norm = "rms"
+    assert abs(O.exit_step(e, x + shift, y).loss - O.exit_step(e, x, y).loss) > 1e-3
+
+
+def test_bias_gradient_reordering_identities():
+    """With a bias: sum_n dZ = W_out^T (sum_n G) and dW_out = (G^T zhat) * gamma +
+    outer(sum_n G, beta): the reorderings the GPU epilogue uses."""
+    rng = np.random.default_rng(82)
+    N, h, V = 11, 10, 23
+    e = rand_layer_exit(O.EXIT_NORM, h, V, 0, rng)
+    x = rng.standard_normal((N, h)) + 0.5
+    y = rng.integers(0, V, N)
+    f = O.exit_forward(e, x)
+    g = O.logit_grad(f["s"], y, np.full(N, 1.0 / N))
+    gsum = g.sum(axis=0)
+    r = O.exit_step(e, x, y)
+    np.testing.assert_allclose(r.grads["beta"], e.w_out.T @ gsum, rtol=1e-12, atol=1e-16)
+    np.testing.assert_allclose(r.grads["w_out"], (g.T @ f["z_hat"]) * e.gamma[None, :] + np.outer(gsum, e.beta),
+                               rtol=1e-12, atol=1e-16)
+    np.testing.assert_allclose(r.grads["gamma"], np.sum(e.w_out * (g.T @ f["z_hat"]), axis=0), rtol=1e-12)
+
+
+def test_layer_workload_recipe():
+    w = W.custom(W.EXIT_NORM, 64, 128, 300, name="ln", norm="layer", bias=True)
+    b = W.make_batch(w, 0)
+    ex = O.exits_from_batch(b)[0]
+    assert ex.norm == "layer" and ex.beta is not None and ex.beta.shape == (128,)
+    x = W.decode(b.hidden[0])
+    assert np.std(x.mean(axis=1)) > 0.5          # row offsets make centring matter
+    w2 = W.custom(W.EXIT_NORM, 64, 128, 300, name="ln")
+    assert O.exits_from_batch(W.make_batch(w2, 0))[0].beta is None

@@ -50,6 +50,8 @@ class Workload:
     row_scale: bool        # per-row lognormal(0, 0.5) scale on X
     zipf: bool             # Zipf(1.1) targets, else uniform
     eps: float = 1e-5      # RMSNorm epsilon (Llama-2 value)
+    norm: str = "rms"      # exit normalisation: "rms" or "layer" (LayerNorm, Norm exits)
+    bias: bool = False     # LayerNorm with a bias beta
 
     @property
     def n_exits(self) -> int:
@@ -74,10 +76,11 @@ WORKLOAD_ORDER = list(WORKLOADS)
 
 def custom(kind: int, n_tokens: int, hidden: int, vocab: int, intermediate: int = 0,
            dtype: str = DTYPE_BF16, exit_weights=(1.0,), row_scale: bool = True,
-           zipf: bool = True, eps: float = 1e-5, name: str = "custom") -> Workload:
+           zipf: bool = True, eps: float = 1e-5, name: str = "custom", norm: str = "rms",
+           bias: bool = False) -> Workload:
     """A workload of arbitrary shape drawn with the same recipe."""
     return Workload(name, kind, n_tokens, hidden, vocab, intermediate, dtype,
-                    tuple(float(w) for w in exit_weights), row_scale, zipf, eps)
+                    tuple(float(w) for w in exit_weights), row_scale, zipf, eps, norm, bias)
 
 
 # ---------------------------------------------------------------- bf16 bits
@@ -143,6 +146,7 @@ class ExitParams:
     kind: int
     w_out: np.ndarray                    # [V][h]
     gamma: Optional[np.ndarray] = None   # [h]   exit norm gain (Norm, MLP)
+    beta: Optional[np.ndarray] = None    # [h]   LayerNorm bias (Norm exit with bias)
     gamma_mlp: Optional[np.ndarray] = None  # [h] MLP pre-norm gain (MLP)
     w_gate: Optional[np.ndarray] = None  # [I][h]
     w_up: Optional[np.ndarray] = None    # [I][h]
@@ -170,7 +174,7 @@ def make_batch(w: Workload, seed: int = 0, random_gamma: bool = False,
     """
     salt = sum((i + 1) * ord(c) for i, c in enumerate(w.name)) & 0xFFFFFFFF
     ss = np.random.SeedSequence([ROOT_SEED, int(seed), salt])
-    n_streams = 2 + w.n_exits * 8
+    n_streams = 2 + w.n_exits * 9
     streams = [np.random.Generator(np.random.PCG64(c)) for c in ss.spawn(n_streams)]
     it = iter(streams)
 
@@ -186,12 +190,16 @@ def make_batch(w: Workload, seed: int = 0, random_gamma: bool = False,
         m[rng_m.random(w.n_tokens) < 0.1] = 0.0   # some masked tokens
 
     hidden, exits = [], []
-    for _ in range(w.n_exits):
-        rx, rs, rw, rg, rgm, rwg, rwu, rwd = (next(it) for _ in range(8))
+    per_exit = [[next(it) for _ in range(8)] for _ in range(w.n_exits)]
+    extra = [next(it) for _ in range(w.n_exits)]     # LayerNorm offsets and bias
+    for (rx, rs, rw, rg, rgm, rwg, rwu, rwd), rb in zip(per_exit, extra):
         x = _normal(rx, (w.n_tokens, w.hidden))
         if w.row_scale:
             s = np.exp(0.5 * rs.standard_normal(w.n_tokens)).astype(np.float32)
             x *= s[:, None]
+        if w.norm == "layer":
+            # a per-row offset, so that the mean-centring of LayerNorm matters
+            x += rb.standard_normal(w.n_tokens).astype(np.float32)[:, None]
         hidden.append(_store(x, w.dtype))
         w_out = _store(_normal(rw, (w.vocab, w.hidden), 0.02), w.dtype)
         p = ExitParams(kind=w.kind, w_out=w_out)
@@ -199,6 +207,8 @@ def make_batch(w: Workload, seed: int = 0, random_gamma: bool = False,
             g = (1.0 + _normal(rg, (w.hidden,), 0.1)) if random_gamma \
                 else np.ones(w.hidden, np.float32)
             p.gamma = _store(g, w.dtype)
+        if w.kind == EXIT_NORM and w.norm == "layer" and w.bias:
+            p.beta = _store(_normal(rb, (w.hidden,), 0.1), w.dtype)
         if w.kind == EXIT_MLP:
             gm = (1.0 + _normal(rgm, (w.hidden,), 0.1)) if random_gamma \
                 else np.ones(w.hidden, np.float32)
