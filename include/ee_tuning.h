@@ -76,6 +76,13 @@ typedef enum ee_exit_kind {
   EE_EXIT_LAYER = 3
 } ee_exit_kind;
 
+/* Normalisation of a Norm exit (Sec. 3.1: "a LayerNorm or RMSNorm module").
+ *  RMS    s_hat = s (mean_j s_j^2 + eps)^(-1/2)                    (default)
+ *  LAYER  s_hat = (s - mean_j s_j) (mean_j (s_j - mean)^2 + eps)^(-1/2),
+ *         z = s_hat * gamma + beta, with beta optional (NULL: no bias).
+ * LAYER is available for NORM exits; MLP exits use RMSNorm. */
+typedef enum ee_norm { EE_NORM_RMS = 0, EE_NORM_LAYER = 1 } ee_norm;
+
 /* Step flags. */
 #define EE_FLAG_DYNAMIC_TOKEN_WEIGHTS 1u
 /* Appendix "Dynamic token-wise loss weighting": weight each token's NLL by
@@ -90,14 +97,15 @@ typedef struct ee_exit {
   int64_t hidden;        /* h: multiple of 64, 64 <= h <= 32768              */
   int64_t vocab;         /* V: 1 <= V <= 1048576                             */
   int64_t intermediate;  /* I (MLP only): multiple of 64, <= 65536; else 0   */
-  float rms_eps;         /* RMSNorm epsilon, >= 0 (Llama-2 uses 1e-5)        */
-  int32_t reserved;      /* must be 0                                        */
+  float rms_eps;         /* norm epsilon, >= 0 (Llama-2 uses 1e-5)           */
+  int32_t norm;          /* ee_norm; EE_NORM_LAYER only for NORM exits       */
   const void *w_out;     /* [V][h]                                           */
   const void *gamma;     /* [h] exit RMSNorm gain (NORM, MLP)                */
   const void *gamma_mlp; /* [h] MLP pre-norm gain (MLP)                      */
   const void *w_gate;    /* [I][h] (MLP)                                     */
   const void *w_up;      /* [I][h] (MLP)                                     */
   const void *w_down;    /* [h][I] (MLP)                                     */
+  const void *beta;      /* [h] LayerNorm bias (NORM + LAYER), or NULL       */
 } ee_exit;
 
 /* Gradients of one exit's parameters, fp32, same shapes as the parameters.
@@ -109,6 +117,7 @@ typedef struct ee_exit_grads {
   float *d_w_gate;
   float *d_w_up;
   float *d_w_down;
+  float *d_beta;         /* required when the exit has a bias                */
 } ee_exit_grads;
 
 /* Bytes of device workspace needed to run the given exits over n_tokens

@@ -35,6 +35,9 @@ EE_EXIT_LAYER = 3
 
 EE_FLAG_DYNAMIC_TOKEN_WEIGHTS = 1
 
+EE_NORM_RMS = 0
+EE_NORM_LAYER = 1
+
 EE_ABI_VERSION = 2
 
 # Every symbol include/ee_tuning.h declares.
@@ -51,10 +54,11 @@ class EeExit(ctypes.Structure):
         ("kind", ctypes.c_int32), ("dtype", ctypes.c_int32),
         ("hidden", ctypes.c_int64), ("vocab", ctypes.c_int64),
         ("intermediate", ctypes.c_int64), ("rms_eps", ctypes.c_float),
-        ("reserved", ctypes.c_int32),
+        ("norm", ctypes.c_int32),
         ("w_out", ctypes.c_void_p), ("gamma", ctypes.c_void_p),
         ("gamma_mlp", ctypes.c_void_p), ("w_gate", ctypes.c_void_p),
         ("w_up", ctypes.c_void_p), ("w_down", ctypes.c_void_p),
+        ("beta", ctypes.c_void_p),
     ]
 
 
@@ -63,6 +67,7 @@ class EeExitGrads(ctypes.Structure):
         ("d_w_out", ctypes.c_void_p), ("d_gamma", ctypes.c_void_p),
         ("d_gamma_mlp", ctypes.c_void_p), ("d_w_gate", ctypes.c_void_p),
         ("d_w_up", ctypes.c_void_p), ("d_w_down", ctypes.c_void_p),
+        ("d_beta", ctypes.c_void_p),
     ]
 
 
@@ -232,15 +237,15 @@ def ee_profile_stop(capacity: int = 64) -> dict:
 # ----------------------------------------------------------- construction
 def make_exit(kind: int, dtype: int, hidden: int, vocab: int, intermediate: int = 0,
               rms_eps: float = 1e-5, w_out=None, gamma=None, gamma_mlp=None, w_gate=None,
-              w_up=None, w_down=None) -> EeExit:
-    return EeExit(kind, dtype, hidden, vocab, intermediate, rms_eps, 0, ptr(w_out), ptr(gamma),
-                  ptr(gamma_mlp), ptr(w_gate), ptr(w_up), ptr(w_down))
+              w_up=None, w_down=None, beta=None, norm: int = EE_NORM_RMS) -> EeExit:
+    return EeExit(kind, dtype, hidden, vocab, intermediate, rms_eps, norm, ptr(w_out), ptr(gamma),
+                  ptr(gamma_mlp), ptr(w_gate), ptr(w_up), ptr(w_down), ptr(beta))
 
 
 def make_grads(d_w_out=None, d_gamma=None, d_gamma_mlp=None, d_w_gate=None, d_w_up=None,
-               d_w_down=None) -> EeExitGrads:
+               d_w_down=None, d_beta=None) -> EeExitGrads:
     return EeExitGrads(ptr(d_w_out), ptr(d_gamma), ptr(d_gamma_mlp), ptr(d_w_gate), ptr(d_w_up),
-                       ptr(d_w_down))
+                       ptr(d_w_down), ptr(d_beta))
 
 
 def adam_tensor(param, grad, exp_avg, exp_avg_sq, master=None, numel: Optional[int] = None,

@@ -45,6 +45,8 @@ struct Layout {
   size_t z = 0, zht = 0, r = 0, P = 0, pm = 0, pl = 0, tgt = 0, lse = 0, sn = 0, bsum = 0, dgp = 0;
   size_t u = 0, uhat = 0, rx = 0, hg = 0, hu = 0, act = 0, y = 0, dz = 0, dy = 0, dhg = 0, dhu = 0,
          dgpg = 0, dgpu = 0;
+  size_t mu = 0, gsp = 0, gsum = 0, dbp = 0;  // LayerNorm mean; bias: G row sums, bias partials
+  int64_t gchunks = 0;
   size_t total = 0;
 };
 constexpr size_t kFlagOff = 0;
@@ -81,6 +83,13 @@ Layout layout(const ee_exit &e, int64_t n) {
   L.sn = take(ldn * 4);
   L.bsum = take(static_cast<size_t>(cdiv64(n, 32)) * 4);
   if (normed) L.dgp = take(static_cast<size_t>(L.vtiles) * h * 4);
+  if (e.norm == EE_NORM_LAYER) L.mu = take(ldn * 4);
+  if (e.beta != nullptr) {
+    L.gchunks = ee::seed_chunks(static_cast<int>(L.ldn));
+    L.gsp = take(static_cast<size_t>(L.gchunks) * V * 4);
+    L.gsum = take(V * 4);
+    L.dbp = take(static_cast<size_t>(L.vtiles) * h * 4);
+  }
   if (e.kind == EE_EXIT_MLP) {
     L.u = take(N * h * es);
     L.uhat = take(N * h * es);
@@ -141,7 +150,13 @@ ee_status validate_exit(const ee_exit *e, int idx) {
   }
   if (!(e->rms_eps >= 0.0f) || !std::isfinite(e->rms_eps))
     return fail(EE_ERR_SHAPE, "exit %d: rms_eps must be finite and >= 0", idx);
-  if (e->reserved != 0) return fail(EE_ERR_SHAPE, "exit %d: reserved field must be 0", idx);
+  if (e->norm != EE_NORM_RMS && e->norm != EE_NORM_LAYER)
+    return fail(EE_ERR_UNSUPPORTED, "exit %d: unknown norm %d", idx, e->norm);
+  if (e->norm == EE_NORM_LAYER && e->kind != EE_EXIT_NORM)
+    return fail(EE_ERR_UNSUPPORTED, "exit %d: LayerNorm is available for Norm exits only", idx);
+  if (e->beta != nullptr && e->norm != EE_NORM_LAYER)
+    return fail(EE_ERR_SHAPE, "exit %d: beta is the bias of a LayerNorm exit", idx);
+  EE_TRY(check_opt_ptr(e->beta, "beta"));
   EE_TRY(check_ptr(e->w_out, "w_out"));
   if (e->kind != EE_EXIT_EMBEDDING) EE_TRY(check_ptr(e->gamma, "gamma"));
   if (e->kind == EE_EXIT_MLP) {
@@ -178,6 +193,7 @@ int grad_ranges(const ee_exit &e, const ee_exit_grads &g, Range *out) {
   int k = 0;
   out[k++] = make_range(g.d_w_out, V * h * 4, "d_w_out");
   if (e.kind != EE_EXIT_EMBEDDING) out[k++] = make_range(g.d_gamma, h * 4, "d_gamma");
+  if (e.beta != nullptr) out[k++] = make_range(g.d_beta, h * 4, "d_beta");
   if (e.kind == EE_EXIT_MLP) {
     out[k++] = make_range(g.d_gamma_mlp, h * 4, "d_gamma_mlp");
     out[k++] = make_range(g.d_w_gate, I * h * 4, "d_w_gate");
@@ -193,6 +209,7 @@ int param_ranges(const ee_exit &e, Range *out) {
   int k = 0;
   out[k++] = make_range(e.w_out, V * h * es, "w_out");
   if (e.kind != EE_EXIT_EMBEDDING) out[k++] = make_range(e.gamma, h * es, "gamma");
+  if (e.beta != nullptr) out[k++] = make_range(e.beta, h * es, "beta");
   if (e.kind == EE_EXIT_MLP) {
     out[k++] = make_range(e.gamma_mlp, h * es, "gamma_mlp");
     out[k++] = make_range(e.w_gate, I * h * es, "w_gate");
@@ -206,6 +223,7 @@ ee_status validate_grads(const ee_exit &e, const ee_exit_grads *g, int idx) {
   if (g == nullptr) return fail(EE_ERR_NULL, "gradient set of exit %d is NULL", idx);
   EE_TRY(check_ptr(g->d_w_out, "d_w_out"));
   if (e.kind != EE_EXIT_EMBEDDING) EE_TRY(check_ptr(g->d_gamma, "d_gamma"));
+  if (e.beta != nullptr) EE_TRY(check_ptr(g->d_beta, "d_beta"));
   if (e.kind == EE_EXIT_MLP) {
     EE_TRY(check_ptr(g->d_gamma_mlp, "d_gamma_mlp"));
     EE_TRY(check_ptr(g->d_w_gate, "d_w_gate"));
@@ -289,9 +307,10 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
                                  nullptr, at(ws, L.zht), s));
     zsrc = at(ws, L.z);
   } else if (e.kind == EE_EXIT_NORM) {
-    EE_LAUNCH("exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s));
+    float *mu = e.norm == EE_NORM_LAYER ? atf(ws, L.mu) : nullptr;
+    EE_LAUNCH("exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s, mu));
     EE_LAUNCH("exit norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.r), e.gamma, n, ldn, h, at(ws, L.z), nullptr,
-                                 at(ws, L.zht), s));
+                                 at(ws, L.zht), s, mu, e.beta));
     zsrc = at(ws, L.z);
   } else {
     EE_LAUNCH("hidden-state transpose", s, ee::launch_norm_apply(f32, f32, x, h, nullptr, nullptr, n, ldn, h, nullptr, nullptr, at(ws, L.zht), s));
@@ -316,7 +335,12 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   a.exit_weight = w_e;
   a.dynamic_weights = (flags & EE_FLAG_DYNAMIC_TOKEN_WEIGHTS) ? 1 : 0;
   EE_LAUNCH("cross-entropy reduce", s, ee::launch_ce_reduce(a, s));
-  EE_LAUNCH("logit seed", s, ee::launch_seed(f32, at(ws, L.P), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), targets, n, ldn, V, L.vtile, s));
+  const bool bias = e.beta != nullptr;
+  EE_LAUNCH("logit seed", s, ee::launch_seed(f32, at(ws, L.P), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), targets, n, ldn, V, L.vtile, s,
+                                             bias ? atf(ws, L.gsp) : nullptr));
+  if (bias)
+    EE_LAUNCH("logit-gradient row sums", s, ee::launch_gain_reduce(atf(ws, L.gsp), static_cast<int>(L.gchunks), nullptr, 0, V,
+                                                                   atf(ws, L.gsum), 0, s));
   EE_LAUNCH("loss reduce", s, ee::launch_final_loss(atf(ws, L.bsum), static_cast<int>(cdiv64(n, 32)), n, loss, total, w_e, first, s));
   return EE_OK;
 }
@@ -328,10 +352,14 @@ ee_status run_backward(const ee_exit &e, int64_t n64, void *ws, const ee_exit_gr
   const int n = static_cast<int>(n64), h = static_cast<int>(e.hidden), V = static_cast<int>(e.vocab);
   const int I = static_cast<int>(e.intermediate), ldn = static_cast<int>(L.ldn);
   const bool normed = e.kind != EE_EXIT_EMBEDDING;
+  const bool bias = e.beta != nullptr;
   EE_LAUNCH("output-matrix gradient", s, ee::gemm_weight_grad_kk(f32, at(ws, L.P), at(ws, L.zht), V, h, ldn, normed ? e.gamma : nullptr,
-                                 normed ? e.w_out : nullptr, g.d_w_out, normed ? atf(ws, L.dgp) : nullptr, acc, s));
+                                 normed ? e.w_out : nullptr, g.d_w_out, normed ? atf(ws, L.dgp) : nullptr, acc, s,
+                                 bias ? atf(ws, L.gsum) : nullptr, e.beta, bias ? atf(ws, L.dbp) : nullptr));
   if (normed)
     EE_LAUNCH("exit gain gradient", s, ee::launch_gain_reduce(atf(ws, L.dgp), static_cast<int>(L.vtiles), nullptr, 0, h, g.d_gamma, acc, s));
+  if (bias)
+    EE_LAUNCH("exit bias gradient", s, ee::launch_gain_reduce(atf(ws, L.dbp), static_cast<int>(L.vtiles), nullptr, 0, h, g.d_beta, acc, s));
   if (e.kind != EE_EXIT_MLP) return EE_OK;
   EE_LAUNCH("dZ", s, ee::gemm_dz(f32, at(ws, L.P), e.w_out, n, ldn, h, V, atf(ws, L.dz), s));
   EE_LAUNCH("exit norm backward", s, ee::launch_norm_bwd(f32, atf(ws, L.dz), atf(ws, L.y), atf(ws, L.r), e.gamma, n, h, at(ws, L.dy), s));
@@ -389,7 +417,7 @@ ee_status check_aliasing(int n_exits, const ee_exit *exits, const void *const *h
 // ------------------------------------------------------------ decode
 // Workspace regions of the decode-time decision for n rows.
 struct DecLayout {
-  size_t z = 0, r = 0, u = 0, rx = 0, hg = 0, act = 0, y = 0, pm = 0, pl = 0, pa = 0, total = 0;
+  size_t z = 0, r = 0, mu = 0, u = 0, rx = 0, hg = 0, act = 0, y = 0, pm = 0, pl = 0, pa = 0, total = 0;
   int tiles = 0;
 };
 
@@ -406,6 +434,7 @@ DecLayout dec_layout(const ee_exit &e, int64_t n) {
   };
   L.z = take(N * h * es);
   L.r = take(N * 4);
+  L.mu = take(N * 4);
   if (e.kind == EE_EXIT_MLP) {
     L.u = take(N * h * es);
     L.rx = take(N * 4);
@@ -451,9 +480,11 @@ ee_status run_decide(const ee_exit &e, const void *x, int64_t n64, float thresho
                                     nullptr, s));
     z = at(ws, L.z);
   } else if (e.kind == EE_EXIT_NORM) {
-    EE_LAUNCH("decode exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s));
+    float *mu = e.norm == EE_NORM_LAYER ? atf(ws, L.mu) : nullptr;
+    EE_LAUNCH("decode exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s, mu));
     EE_LAUNCH("decode exit norm apply", s,
-              ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.r), e.gamma, n, n, h, at(ws, L.z), nullptr, nullptr, s));
+              ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.r), e.gamma, n, n, h, at(ws, L.z), nullptr, nullptr, s, mu,
+                                    e.beta));
     z = at(ws, L.z);
   }
   int32_t *pa = reinterpret_cast<int32_t *>(at(ws, L.pa));

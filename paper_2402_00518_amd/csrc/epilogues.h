@@ -153,6 +153,9 @@ struct EpiLogits {
 // The partials sum over tiles to the gain's gradient, because
 //   sum_n dZ[n][j] x_hat[n][j] = sum_r W[r][j] (G^T x_hat)[r][j],
 // the same triple sum reordered; no dZ GEMM is needed for it.
+// With a LayerNorm bias b (z = x_hat * gain + b), Z = X_hat * gain + 1 b^T, so
+//   dW[r][j]       += gsum[r] * b[j]               (gsum[r] = sum_n G[n][r])
+//   part_b[tile][j] = sum_{r in tile} W[r][j] * gsum[r]   (sums to d b)
 template <typename T>
 struct EpiWeightGrad {
   struct Params {
@@ -162,36 +165,57 @@ struct EpiWeightGrad {
     const T *W;         // [M][ldw] or NULL (no gain-gradient partials)
     float *part;        // [tiles over M][ldw]
     int accumulate;
+    const float *gsum;  // [M] with a bias, else NULL
+    const T *bias;      // [N] or NULL
+    float *part_b;      // [tiles over M][ldw] with a bias
+  };
+  struct In {
+    float w, old, gs;
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
     constexpr int NB = Cfg::NB;
-    float g[NB], dg[NB];
+    float g[NB], dg[NB], bt[NB], db[NB];
     with_flag(p.gain != nullptr, [&](auto G_) EE_ALWAYS_INLINE {
       static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
         g[j] = decltype(G_)::value ? to_f32(p.gain[min(t.col(j), t.N - 1)]) : 1.0f;
         dg[j] = 0.0f;
+        db[j] = 0.0f;
+        bt[j] = 0.0f;
       });
     });
     const bool with_w = p.W != nullptr;
+    const bool with_b = p.bias != nullptr;
+    if (with_b) static_for<NB>([&](auto j) EE_ALWAYS_INLINE { bt[j] = to_f32(p.bias[min(t.col(j), t.N - 1)]); });
+    auto body = [&](auto W_, auto A_, auto B_) EE_ALWAYS_INLINE {
+          constexpr bool kW = decltype(W_)::value, kAcc = decltype(A_)::value, kB = decltype(B_)::value;
+          for_each_acc_loaded<Cfg>(
+              acc, t, t.M, t.N,
+              [&](int row, int col) EE_ALWAYS_INLINE {
+                const int64_t o = static_cast<int64_t>(row) * p.ldw + col;
+                In r{0.0f, 0.0f, 0.0f};
+                if constexpr (kW) r.w = to_f32(p.W[o]);
+                if constexpr (kAcc) r.old = p.dW[o];
+                if constexpr (kB) r.gs = p.gsum[row];
+                return r;
+              },
+              [&](int row, int col, int j, float c, In in) EE_ALWAYS_INLINE {
+                if (row < t.M && col < t.N) {
+                  float v = in.old + c * g[j];
+                  if constexpr (kB) v += in.gs * bt[j];
+                  p.dW[static_cast<int64_t>(row) * p.ldw + col] = v;
+                  if constexpr (kW) dg[j] += in.w * c;
+                  if constexpr (kW && kB) db[j] += in.w * in.gs;
+                }
+              });
+    };
+    // A bias comes with W (the bias gradient needs W): six variants.
     with_flag(with_w, [&](auto W_) EE_ALWAYS_INLINE {
       with_flag(p.accumulate != 0, [&](auto A_) EE_ALWAYS_INLINE {
-        constexpr bool kW = decltype(W_)::value, kAcc = decltype(A_)::value;
-        for_each_acc_loaded<Cfg>(
-            acc, t, t.M, t.N,
-            [&](int row, int col) EE_ALWAYS_INLINE {
-              const int64_t o = static_cast<int64_t>(row) * p.ldw + col;
-              F2 r{0.0f, 0.0f};
-              if constexpr (kW) r.a = to_f32(p.W[o]);
-              if constexpr (kAcc) r.b = p.dW[o];
-              return r;
-            },
-            [&](int row, int col, int j, float c, F2 in) EE_ALWAYS_INLINE {
-              if (row < t.M && col < t.N) {
-                p.dW[static_cast<int64_t>(row) * p.ldw + col] = in.b + c * g[j];
-                if constexpr (kW) dg[j] += in.a * c;
-              }
-            });
+        if constexpr (decltype(W_)::value)
+          with_flag(with_b, [&](auto B_) EE_ALWAYS_INLINE { body(W_, A_, B_); });
+        else
+          body(W_, A_, std::false_type{});
       });
     });
     if (with_w) {
@@ -201,6 +225,15 @@ struct EpiWeightGrad {
           const int col = t.col(j);
           if (col < t.N) p.part[static_cast<int64_t>(t.tile_m) * p.ldw + col] = dg[j];
         });
+      }
+      if (with_b) {
+        tile_col_reduce<false, Cfg>(t, db);
+        if (t.wave_m == 0 && t.lane < 32) {
+          static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
+            const int col = t.col(j);
+            if (col < t.N) p.part_b[static_cast<int64_t>(t.tile_m) * p.ldw + col] = db[j];
+          });
+        }
       }
     }
   }

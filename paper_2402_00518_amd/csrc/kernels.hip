@@ -67,24 +67,43 @@ template <int N> __device__ __forceinline__ void store_f32(bf16_t *p, const floa
   }
 }
 
-// -------------------------------------------------------------- RMSNorm
-// One wave per row; fp32 sum of squares reduced across the wave.
+// ------------------------------------------------------- row statistics
+// One wave per row.  RMSNorm: r = (mean x^2 + eps)^(-1/2).  LayerNorm (mu
+// given): mu = mean x, then r = (mean (x - mu)^2 + eps)^(-1/2) from a second
+// pass over the row (no cancellation from subtracting squared means).
 template <typename Tin>
 __global__ __launch_bounds__(256) void row_rms_kernel(const Tin *x, int64_t ldx, int n, int h, float eps,
-                                                      float *r) {
+                                                      float *r, float *mu) {
   constexpr int V = 16 / sizeof(Tin);
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= n) return;
   const Tin *xr = x + static_cast<int64_t>(row) * ldx;
+  float mean = 0.0f;
+  if (mu != nullptr) {
+    float t = 0.0f;
+    for (int j = lane * V; j < h; j += kWave * V) {
+      float v[V];
+      load_f32<V>(xr + j, v);
+#pragma unroll
+      for (int e = 0; e < V; ++e) t += v[e];
+    }
+    mean = warp_sum(t) / static_cast<float>(h);
+  }
   float s = 0.0f;
   for (int j = lane * V; j < h; j += kWave * V) {
     float v[V];
     load_f32<V>(xr + j, v);
 #pragma unroll
-    for (int e = 0; e < V; ++e) s += v[e] * v[e];
+    for (int e = 0; e < V; ++e) {
+      const float c = v[e] - mean;
+      s += c * c;
+    }
   }
   s = warp_sum(s);
-  if (lane == 0) r[row] = 1.0f / sqrtf(s / static_cast<float>(h) + eps);
+  if (lane == 0) {
+    r[row] = 1.0f / sqrtf(s / static_cast<float>(h) + eps);
+    if (mu != nullptr) mu[row] = mean;
+  }
 }
 
 // 64 tokens x 64 features per block.  Row-major outputs are written
@@ -92,8 +111,8 @@ __global__ __launch_bounds__(256) void row_rms_kernel(const Tin *x, int64_t ldx,
 // transpose so that both sides are coalesced.
 template <typename Tin, typename T>
 __global__ __launch_bounds__(256) void norm_apply_kernel(const Tin *x, int64_t ldx, const float *r,
-                                                         const T *gain, int n, int ldn, int h, T *z,
-                                                         T *x_hat, T *x_hat_t) {
+                                                         const float *mu, const T *gain, const T *bias, int n,
+                                                         int ldn, int h, T *z, T *x_hat, T *x_hat_t) {
   __shared__ float tile[64][65];
   const int n0 = blockIdx.x * 64, j0 = blockIdx.y * 64;
   const int tid = threadIdx.x;
@@ -103,8 +122,9 @@ __global__ __launch_bounds__(256) void norm_apply_kernel(const Tin *x, int64_t l
   if (row < n) {
     load_f32<16>(x + static_cast<int64_t>(row) * ldx + j0 + tc, v);
     const float rs = r != nullptr ? r[row] : 1.0f;
+    const float m = mu != nullptr ? mu[row] : 0.0f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) v[e] *= rs;
+    for (int e = 0; e < 16; ++e) v[e] = (v[e] - m) * rs;
     const int64_t o = static_cast<int64_t>(row) * h + j0 + tc;
     if (x_hat != nullptr) store_f32<16>(x_hat + o, v);
     if (z != nullptr) {
@@ -117,6 +137,12 @@ __global__ __launch_bounds__(256) void norm_apply_kernel(const Tin *x, int64_t l
       } else {
 #pragma unroll
         for (int e = 0; e < 16; ++e) zz[e] = v[e];
+      }
+      if (bias != nullptr) {
+        float b[16];
+        load_f32<16>(bias + j0 + tc, b);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) zz[e] += b[e];
       }
       store_f32<16>(z + o, zz);
     }
@@ -217,9 +243,10 @@ __global__ __launch_bounds__(256) void ce_reduce_kernel(CeReduceArgs a) {
 template <typename T>
 __global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, const float *lse,
                                                    const float *sn, const int32_t *targets, int n,
-                                                   int ldn, int vocab, int vtile) {
+                                                   int ldn, int vocab, int vtile, float *gsum_part) {
+  __shared__ float red[16][4];
   const int c0 = blockIdx.y * 2048 + threadIdx.x * 8;
-  if (c0 >= ldn) return;
+  if (gsum_part == nullptr && c0 >= ldn) return;
   const int v0 = blockIdx.x * 16;
   const int tile = v0 / vtile;
   float cf[8], s[8];
@@ -238,22 +265,39 @@ __global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, co
   // vectors; converted at use).
   constexpr int VEC = 8 * sizeof(T) / 16;  // 16-byte vectors per 8 values
   u32x4_t raw[16][VEC];
+  const int cl = min(c0, ldn - 8);  // threads past ldn (kept for the row sums) re-read the last chunk
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    const u32x4_t *src = reinterpret_cast<const u32x4_t *>(P + static_cast<int64_t>(v0 + min(r, rows - 1)) * ldn + c0);
+    const u32x4_t *src = reinterpret_cast<const u32x4_t *>(P + static_cast<int64_t>(v0 + min(r, rows - 1)) * ldn + cl);
 #pragma unroll
     for (int q = 0; q < VEC; ++q) raw[r][q] = src[q];
   }
+  float rsum[16];
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    if (r < rows) {
-      float p[8], g[8];
-      load_f32<8>(reinterpret_cast<const T *>(raw[r]), p);
+    float p[8], g[8];
+    load_f32<8>(reinterpret_cast<const T *>(raw[r]), p);
+    rsum[r] = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) g[e] = ok[e] ? p[e] * cf[e] - (yy[e] == v0 + r ? s[e] : 0.0f) : 0.0f;
-      store_f32<8>(P + static_cast<int64_t>(v0 + r) * ldn + c0, g);
+    for (int e = 0; e < 8; ++e) {
+      g[e] = ok[e] ? p[e] * cf[e] - (yy[e] == v0 + r ? s[e] : 0.0f) : 0.0f;
+      rsum[r] += g[e];
     }
+    if (r < rows && c0 < ldn) store_f32<8>(P + static_cast<int64_t>(v0 + r) * ldn + c0, g);
   }
+  // Row sums of G over this block's tokens (LayerNorm bias gradient): fp32,
+  // fixed order (wave sums, then the 4 waves in order).
+  if (gsum_part == nullptr) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const float t = warp_sum(rsum[r]);
+    if (lane == 0) red[r][wave] = t;
+  }
+  __syncthreads();
+  if (threadIdx.x < rows)
+    gsum_part[static_cast<int64_t>(blockIdx.y) * vocab + v0 + threadIdx.x] =
+        ((red[threadIdx.x][0] + red[threadIdx.x][1]) + red[threadIdx.x][2]) + red[threadIdx.x][3];
 }
 
 __global__ __launch_bounds__(256) void final_loss_kernel(const float *bs, int nb, int n, float *loss,
@@ -308,30 +352,32 @@ __global__ void clear_flag_kernel(int *flag) { *flag = 0; }
   } while (0)
 
 hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps, float *r,
-                          hipStream_t stream) {
+                          hipStream_t stream, float *mu) {
   const dim3 grid(cdiv(n, 4));
   if (x_f32)
     hipLaunchKernelGGL(row_rms_kernel<float>, grid, dim3(256), 0, stream, static_cast<const float *>(x), ldx,
-                       n, h, eps, r);
+                       n, h, eps, r, mu);
   else
     hipLaunchKernelGGL(row_rms_kernel<bf16_t>, grid, dim3(256), 0, stream, static_cast<const bf16_t *>(x),
-                       ldx, n, h, eps, r);
+                       ldx, n, h, eps, r, mu);
   return hipGetLastError();
 }
 
 hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, const float *r,
                              const void *gain, int n, int ldn, int h, void *z, void *x_hat, void *x_hat_t,
-                             hipStream_t stream) {
+                             hipStream_t stream, const float *mu, const void *bias) {
   const dim3 grid(cdiv(ldn, 64), h / 64);
   EE_DISPATCH(f32, {
     if (x_f32)
       hipLaunchKernelGGL((norm_apply_kernel<float, T>), grid, dim3(256), 0, stream,
-                         static_cast<const float *>(x), ldx, r, static_cast<const T *>(gain), n, ldn, h,
-                         static_cast<T *>(z), static_cast<T *>(x_hat), static_cast<T *>(x_hat_t));
+                         static_cast<const float *>(x), ldx, r, mu, static_cast<const T *>(gain),
+                         static_cast<const T *>(bias), n, ldn, h, static_cast<T *>(z), static_cast<T *>(x_hat),
+                         static_cast<T *>(x_hat_t));
     else
       hipLaunchKernelGGL((norm_apply_kernel<bf16_t, T>), grid, dim3(256), 0, stream,
-                         static_cast<const bf16_t *>(x), ldx, r, static_cast<const T *>(gain), n, ldn, h,
-                         static_cast<T *>(z), static_cast<T *>(x_hat), static_cast<T *>(x_hat_t));
+                         static_cast<const bf16_t *>(x), ldx, r, mu, static_cast<const T *>(gain),
+                         static_cast<const T *>(bias), n, ldn, h, static_cast<T *>(z), static_cast<T *>(x_hat),
+                         static_cast<T *>(x_hat_t));
   });
   return hipGetLastError();
 }
@@ -341,11 +387,14 @@ hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+int seed_chunks(int ldn) { return cdiv(ldn, 2048); }
+
 hipError_t launch_seed(bool f32, void *P, const float *part_m, const float *lse, const float *sn,
-                       const int32_t *targets, int n, int ldn, int vocab, int vtile, hipStream_t stream) {
-  const dim3 grid(cdiv(vocab, 16), cdiv(ldn, 2048));
+                       const int32_t *targets, int n, int ldn, int vocab, int vtile, hipStream_t stream,
+                       float *gsum_part) {
+  const dim3 grid(cdiv(vocab, 16), seed_chunks(ldn));
   EE_DISPATCH(f32, hipLaunchKernelGGL(seed_kernel<T>, grid, dim3(256), 0, stream, static_cast<T *>(P), part_m,
-                                      lse, sn, targets, n, ldn, vocab, vtile));
+                                      lse, sn, targets, n, ldn, vocab, vtile, gsum_part));
   return hipGetLastError();
 }
 
@@ -404,10 +453,10 @@ hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, in
 
 hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, int m, int h, int ldn,
                                const void *gain, const void *w, float *dw, float *part, int accumulate,
-                               hipStream_t stream) {
+                               hipStream_t stream, const float *gsum, const void *bias, float *part_b) {
   EE_DISPATCH(f32, {
-    typename EpiWeightGrad<T>::Params ep{dw, h, static_cast<const T *>(gain), static_cast<const T *>(w), part,
-                                         accumulate};
+    typename EpiWeightGrad<T>::Params ep{dw,   h,         static_cast<const T *>(gain), static_cast<const T *>(w),
+                                         part, accumulate, gsum, static_cast<const T *>(bias), part_b};
     return run_gemm<T, true, true, EpiWeightGrad<T>>(Operand{g_t, ldn}, Operand{xhat_t, ldn},
                                                         GemmShape{m, h, ldn}, ep, stream);
   });

@@ -14,16 +14,21 @@ constexpr int kTokenPad = 64;     // padding of the token dimension
 // softmax and gain-gradient partials come one per tile row-block).
 int gemm_tile_rows(bool f32, bool a_kmajor, bool b_kmajor);
 
-// Row-wise RMSNorm scale r[n] = (mean_j x[n][j]^2 + eps)^(-1/2).
+// Row statistics of the exit norm.  RMSNorm (mu == NULL): r[n] =
+// (mean_j x[n][j]^2 + eps)^(-1/2).  LayerNorm: mu[n] = mean_j x[n][j] and
+// r[n] = (mean_j (x[n][j] - mu[n])^2 + eps)^(-1/2).
 hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps,
-                          float *r, hipStream_t stream);
+                          float *r, hipStream_t stream, float *mu = nullptr);
 
-// Apply a row scale and a gain: x_hat = x * r[n] (r == NULL: x_hat = x), z = x_hat * gain.
-// Writes any of z [n][h], x_hat [n][h] (row-major) and x_hat^T [h][ldn]
-// (token-contiguous, columns n..ldn-1 zero).  Output element type = `f32`.
+// Apply the row statistics, a gain and a bias: x_hat = (x - mu[n]) * r[n]
+// (mu == NULL: no centring; r == NULL: no scale), z = x_hat * gain + bias
+// (bias may be NULL).  Writes any of z [n][h], x_hat [n][h] (row-major) and
+// x_hat^T [h][ldn] (token-contiguous, columns n..ldn-1 zero).  Output
+// element type = `f32`.
 hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, const float *r,
                              const void *gain, int n, int ldn, int h, void *z, void *x_hat,
-                             void *x_hat_t, hipStream_t stream);
+                             void *x_hat_t, hipStream_t stream, const float *mu = nullptr,
+                             const void *bias = nullptr);
 
 // Combine the per-tile softmax partials of each token into LSE, the row NLL
 // and the loss weight s_n.  Also flags targets outside [0, V).
@@ -45,9 +50,12 @@ struct CeReduceArgs {
 hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream);
 
 // In place: G[v][n] = P[v][n] * s_n exp(m[v / vtile][n] - LSE_n) - (v == y_n) * s_n
-// (0 for n >= N).
+// (0 for n >= N).  With gsum_part, also the fp32 row sums of G over each
+// chunk of 2048 tokens: gsum_part[chunk][v] (seed_chunks(ldn) chunks).
+int seed_chunks(int ldn);
 hipError_t launch_seed(bool f32, void *P, const float *part_m, const float *lse, const float *sn,
-                       const int32_t *targets, int n, int ldn, int vocab, int vtile, hipStream_t stream);
+                       const int32_t *targets, int n, int ldn, int vocab, int vtile, hipStream_t stream,
+                       float *gsum_part = nullptr);
 
 // loss[0] = sum(block_sums) / n;  total[0] = (first ? 0 : total[0]) + w * loss[0].
 hipError_t launch_final_loss(const float *block_sums, int blocks, int n, float *loss, float *total,
@@ -70,10 +78,12 @@ hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, in
                        int ldn, float *part_m, float *part_l, float *tgt, const int32_t *targets,
                        hipStream_t stream);
 // dW[M][h] = (G^T X_hat) * gain with gain-gradient partials (K = tokens, both operands
-// token-contiguous with leading dimension ldn).
+// token-contiguous with leading dimension ldn).  With a LayerNorm bias:
+// dW += gsum b^T and bias-gradient partials part_b (gsum[v] = sum_n G[n][v]).
 hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, int m, int h, int ldn,
                                const void *gain, const void *w, float *dw, float *part, int accumulate,
-                               hipStream_t stream);
+                               hipStream_t stream, const float *gsum = nullptr, const void *bias = nullptr,
+                               float *part_b = nullptr);
 // Same, operands stored row-major over tokens: g [n][m], xhat [n][h].
 hipError_t gemm_weight_grad_mn(bool f32, const void *g, const void *xhat, int m, int h, int n,
                                const void *gain, const void *w, float *dw, float *part, int accumulate,

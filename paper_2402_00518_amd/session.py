@@ -39,7 +39,7 @@ class Session:
                  eps: float, exits: Sequence[dict], hidden_states: Sequence[np.ndarray],
                  targets: np.ndarray, token_weights: Optional[np.ndarray] = None,
                  exit_weights: Sequence[float] = (1.0,), device: str = "cuda:0",
-                 kinds: Optional[Sequence[int]] = None):
+                 kinds: Optional[Sequence[int]] = None, norm: int = B.EE_NORM_RMS):
         self.device = torch.device(device)
         self.n_tokens = int(len(targets))
         self.hidden, self.vocab, self.intermediate = hidden, vocab, intermediate
@@ -55,10 +55,12 @@ class Session:
             t = {name: to_device(a, self.device) for name, a in p.items() if a is not None}
             self.params.append(t)
             inter = intermediate if k == B.EE_EXIT_MLP else 0
-            self.c_exits.append(B.make_exit(k, dtype, hidden, vocab, inter, eps, **t))
+            self.c_exits.append(B.make_exit(k, dtype, hidden, vocab, inter, eps, norm=norm, **t))
             g = {"d_w_out": torch.zeros(vocab, hidden, dtype=torch.float32, device=self.device)}
             if k != B.EE_EXIT_EMBEDDING:
                 g["d_gamma"] = torch.zeros(hidden, dtype=torch.float32, device=self.device)
+            if "beta" in t:
+                g["d_beta"] = torch.zeros(hidden, dtype=torch.float32, device=self.device)
             if k == B.EE_EXIT_MLP:
                 g["d_gamma_mlp"] = torch.zeros(hidden, dtype=torch.float32, device=self.device)
                 g["d_w_gate"] = torch.zeros(intermediate, hidden, dtype=torch.float32, device=self.device)
@@ -86,10 +88,11 @@ class Session:
         exits = []
         for p in batch.exits:
             d = {"w_out": p.w_out, "gamma": p.gamma, "gamma_mlp": p.gamma_mlp,
-                 "w_gate": p.w_gate, "w_up": p.w_up, "w_down": p.w_down}
+                 "w_gate": p.w_gate, "w_up": p.w_up, "w_down": p.w_down, "beta": p.beta}
             exits.append({k: v for k, v in d.items() if v is not None})
+        norm = B.EE_NORM_LAYER if w.norm == "layer" else B.EE_NORM_RMS
         return cls(w.kind, dtype, w.hidden, w.vocab, w.intermediate, w.eps, exits, batch.hidden,
-                   batch.targets, batch.token_weights, w.exit_weights, device)
+                   batch.targets, batch.token_weights, w.exit_weights, device, norm=norm)
 
     # ------------------------------------------------------------ ABI calls
     def step(self, flags: int = 0, accumulate: int = 0, stream: Optional[int] = None):

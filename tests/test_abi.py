@@ -99,7 +99,8 @@ def test_workspace_bytes():
     ("intermediate", 64, B.EE_ERR_SHAPE, "intermediate"),
     ("rms_eps", -1.0, B.EE_ERR_SHAPE, "rms_eps"),
     ("rms_eps", float("nan"), B.EE_ERR_SHAPE, "rms_eps"),
-    ("reserved", 1, B.EE_ERR_SHAPE, "reserved"),
+    ("norm", 5, B.EE_ERR_UNSUPPORTED, "norm"),
+    ("beta", 0x10_8000_0000, B.EE_ERR_SHAPE, "beta"),            # a bias without LayerNorm
     ("w_out", None, B.EE_ERR_NULL, "w_out"),
     ("gamma", None, B.EE_ERR_NULL, "gamma"),
     ("w_out", 0x10_0000_0008, B.EE_ERR_ALIGN, "w_out"),
@@ -108,6 +109,26 @@ def test_forward_rejects_bad_exit(field, value, code, needle):
     e = fake_exit()
     setattr(e, field, value)
     expect(fwd(e), code, needle)
+
+
+def test_layernorm_is_for_norm_exits_and_needs_a_bias_gradient():
+    e = fake_exit(B.EE_EXIT_MLP, I=512)
+    e.norm = B.EE_NORM_LAYER
+    expect(fwd(e), B.EE_ERR_UNSUPPORTED, "LayerNorm")
+    e = fake_exit(B.EE_EXIT_EMBEDDING)
+    e.norm = B.EE_NORM_LAYER
+    expect(fwd(e), B.EE_ERR_UNSUPPORTED, "LayerNorm")
+    e = fake_exit()
+    e.norm = B.EE_NORM_LAYER
+    e.beta = 0x10_8000_0008
+    expect(fwd(e), B.EE_ERR_ALIGN, "beta")
+    e.beta = 0x10_8000_0000
+    expect(fwd(e, ws_bytes=16), B.EE_ERR_WORKSPACE, "workspace")        # a valid LayerNorm exit
+    assert B.ee_workspace_bytes([e], 100) > B.ee_workspace_bytes([fake_exit()], 100)
+    g = fake_grads()
+    g.d_beta = None
+    st = B.ee_head_backward(e, 100, 0x60_0000_0000, 1 << 32, g, 0, None, check=False)
+    expect(st, B.EE_ERR_NULL, "d_beta")
 
 
 def test_mlp_exit_needs_its_weights():

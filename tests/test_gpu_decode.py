@@ -31,8 +31,9 @@ def say(msg):
     print(msg, flush=True)
 
 
-def make_case(kind, n, h, V, I, dtype, seed):
-    w = W.custom(kind, n, h, V, I, dtype, (1.0,), row_scale=True, zipf=True, name="decode")
+def make_case(kind, n, h, V, I, dtype, seed, norm="rms", bias=False):
+    w = W.custom(kind, n, h, V, I, dtype, (1.0,), row_scale=True, zipf=True, name="decode",
+                 norm=norm, bias=bias)
     b = W.make_batch(w, seed, random_gamma=True)
     return w, b
 
@@ -41,11 +42,12 @@ def run_decide(b, threshold, dev_params=None):
     w = b.workload
     p = b.exits[0]
     d = {"w_out": p.w_out, "gamma": p.gamma, "gamma_mlp": p.gamma_mlp, "w_gate": p.w_gate,
-         "w_up": p.w_up, "w_down": p.w_down}
+         "w_up": p.w_up, "w_down": p.w_down, "beta": p.beta}
     t = dev_params or {k: to_device(a, "cuda") for k, a in d.items() if a is not None}
     dtype = B.EE_F32 if w.dtype == "f32" else B.EE_BF16
     inter = w.intermediate if w.kind == B.EE_EXIT_MLP else 0
-    e = B.make_exit(w.kind, dtype, w.hidden, w.vocab, inter, w.eps, **t)
+    norm = B.EE_NORM_LAYER if w.norm == "layer" else B.EE_NORM_RMS
+    e = B.make_exit(w.kind, dtype, w.hidden, w.vocab, inter, w.eps, norm=norm, **t)
     n = w.n_tokens
     x = to_device(b.hidden[0], "cuda")
     ws_bytes = B.ee_decode_workspace_bytes(e, n)
@@ -105,13 +107,16 @@ CASES = [
     ("norm_f32", W.EXIT_NORM, 6, 64, 333, 0, "f32"),
     ("mlp_f32", W.EXIT_MLP, 33, 128, 300, 192, "f32"),
     ("embedding_f32", W.EXIT_EMBEDDING, 2, 64, 129, 0, "f32"),
+    ("layernorm_bias", W.EXIT_NORM, 9, 192, 1000, 0, "bf16"),
+    ("layernorm_bias_f32", W.EXIT_NORM, 4, 64, 333, 0, "f32"),
 ]
 
 
 @pytest.mark.parametrize("name,kind,n,h,v,inter,dtype", CASES, ids=[c[0] for c in CASES])
 def test_small_decode_parity(name, kind, n, h, v, inter, dtype):
     say(f"case: decode {name} rows={n} h={h} V={v} I={inter} {dtype}")
-    w, b = make_case(kind, n, h, v, inter, dtype, seed=21)
+    norm, bias = ("layer", True) if name.startswith("layernorm") else ("rms", False)
+    w, b = make_case(kind, n, h, v, inter, dtype, seed=21, norm=norm, bias=bias)
     ex = O.exits_from_batch(b)[0]
     conf = D.exit_decide(ex, W.decode(b.hidden[0]), 0.5)["confidence"]
     thr = float(np.median(conf)) if n > 1 else 0.5

@@ -83,8 +83,9 @@ def compare_full(sess, batch, loss_rtol=LOSS_RTOL, grad_rtol=GRAD_RTOL, dynamic=
 
 
 def small(kind, n, h, v, inter=0, dtype="bf16", weights=(1.0,), seed=0, random_gamma=True,
-          token_weights=False, name="small"):
-    w = W.custom(kind, n, h, v, inter, dtype, weights, row_scale=True, zipf=True, name=name)
+          token_weights=False, name="small", norm="rms", bias=False):
+    w = W.custom(kind, n, h, v, inter, dtype, weights, row_scale=True, zipf=True, name=name,
+                 norm=norm, bias=bias)
     return W.make_batch(w, seed, random_gamma=random_gamma, token_weights=token_weights)
 
 
@@ -121,6 +122,25 @@ def test_small_full_parity(name, kind, n, h, v, inter, dtype, tokw):
     s = run(b)
     tight = dtype == "f32"
     compare_full(s, b, loss_rtol=1e-5 if tight else LOSS_RTOL, grad_rtol=1e-4 if tight else GRAD_RTOL)
+
+
+LAYERNORM_CASES = [
+    ("layernorm_bias", 300, 192, 1000, "bf16", True, False),
+    ("layernorm_no_bias", 300, 192, 1000, "bf16", False, False),
+    ("layernorm_bias_tokw_multi_tile", 1000, 512, 2000, "bf16", True, True),
+    ("layernorm_bias_f32", 70, 64, 333, "f32", True, False),
+]
+
+
+@pytest.mark.parametrize("name,n,h,v,dtype,bias,tokw", LAYERNORM_CASES, ids=[c[0] for c in LAYERNORM_CASES])
+def test_layernorm_exit_parity(name, n, h, v, dtype, bias, tokw):
+    # The LayerNorm flavour of the Norm exit (Sec. 3.1), with and without bias.
+    say(f"case: {name} N={n} h={h} V={v} {dtype}")
+    b = small(W.EXIT_NORM, n, h, v, 0, dtype, seed=4, token_weights=tokw, name=name, norm="layer", bias=bias)
+    s = run(b)
+    tight = dtype == "f32"
+    _, per = compare_full(s, b, loss_rtol=1e-5 if tight else LOSS_RTOL, grad_rtol=1e-4 if tight else GRAD_RTOL)
+    assert ("beta" in per[0].grads) == bias
 
 
 def test_row_losses_match():
@@ -258,6 +278,8 @@ def sampled_compare(name, seed=0, random_gamma=False):
         checks = [("d_w_out rows", host(g["d_w_out"][torch.as_tensor(v_rows).cuda()]), ref["w_out_rows"])]
         if ex.kind != W.EXIT_EMBEDDING:
             checks.append(("d_gamma", host(g["d_gamma"]), ref["gamma"]))
+        if ex.beta is not None:
+            checks.append(("d_beta", host(g["d_beta"]), ref["beta"]))
         if ex.kind == W.EXIT_MLP:
             ir = torch.as_tensor(i_rows).cuda()
             checks += [("d_gamma_mlp", host(g["d_gamma_mlp"]), ref["gamma_mlp"]),
@@ -271,7 +293,8 @@ def sampled_compare(name, seed=0, random_gamma=False):
     assert abs(s.loss_total.item() - total) <= LOSS_RTOL * abs(total)
 
 
-@pytest.mark.parametrize("name", ["llama7b_norm", "llama7b_norm_2exits", "llama13b_mlp", "llama70b_norm"])
+@pytest.mark.parametrize("name", ["llama7b_norm", "llama7b_norm_2exits", "llama13b_mlp", "llama70b_norm",
+                                  "llama7b_layernorm"])
 def test_full_size_sampled_parity(name):
     sampled_compare(name)
 

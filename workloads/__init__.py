@@ -70,6 +70,9 @@ WORKLOADS: Dict[str, Workload] = {
                              DTYPE_BF16, (1.0,), True, True),
     "llama70b_norm": Workload("llama70b_norm", EXIT_NORM, 8192, 8192, 32000, 0,
                               DTYPE_BF16, (1.0,), True, True),
+    # the LayerNorm flavour of the Norm exit (with bias) at the 7B shape
+    "llama7b_layernorm": Workload("llama7b_layernorm", EXIT_NORM, 4096, 4096, 32000, 0,
+                                  DTYPE_BF16, (1.0,), True, True, norm="layer", bias=True),
 }
 WORKLOAD_ORDER = list(WORKLOADS)
 
