@@ -461,8 +461,11 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
   //     those writes just drained.
   // A wave issues in order, so bursts of memory instructions would hold up
   // its MFMAs; spread out, they issue while the matrix core is busy.  The
-  // code of a stage has no branches (loads past the last stage re-read it),
-  // so the scheduler sees each stage as one region.  One barrier per stage.
+  // writes of stage kt + 1 are finished by the second-to-last substep; the
+  // barrier follows it, and the last substep then reads the first fragments
+  // of stage kt + 1 while its own MFMAs run, so no stage starts by waiting
+  // for LDS.  The code of a stage has no branches (loads past the last
+  // stage re-read it), so the scheduler sees each stage as one region.
   constexpr int B_OFF = Cfg::BM * kRowBytes;
   const int nk = cdiv(s.K, BK);
   const int a_row0 = wave_m * Cfg::WM, b_row0 = wave_n * Cfg::WN;
@@ -480,31 +483,43 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
     lb.template load<decltype(g)::value>(b_ptr, B.ld, n0, k1);
   });
   __syncthreads();
+  F f0, f1;
+  f0.load(smem, smem + B_OFF, a_row0, b_row0, lane, 0);
   for (int kt = 0; kt < nk; ++kt) {
     const char *cur = smem + (kt & 1) * Cfg::STAGE_BYTES;
     char *next = smem + ((kt + 1) & 1) * Cfg::STAGE_BYTES;
     const int k2 = min(kt + 2, nk - 1) * BK;
-    F f0, f1;
-    f0.load(cur, cur + B_OFF, a_row0, b_row0, lane, 0);
     static_for<SUB>([&](auto st) EE_ALWAYS_INLINE {
       constexpr int sub = decltype(st)::value;
       F &now = (sub % 2 == 0) ? f0 : f1;
       F &later = (sub % 2 == 0) ? f1 : f0;
-      if constexpr (sub + 1 < SUB) later.load(cur, cur + B_OFF, a_row0, b_row0, lane, sub + 1);
-      la.template store<sub>(next, tid);
-      lb.template store<sub>(next + B_OFF, tid);
-      la.template load<sub>(a_ptr, A.ld, m0, k2);
-      lb.template load<sub>(b_ptr, B.ld, n0, k2);
+      if constexpr (sub + 1 < SUB)
+        later.load(cur, cur + B_OFF, a_row0, b_row0, lane, sub + 1);
+      else
+        later.load(next, next + B_OFF, a_row0, b_row0, lane, 0);  // next stage, published by the barrier
+      if constexpr (sub < SUB - 2) {
+        la.template store<sub>(next, tid);
+        lb.template store<sub>(next + B_OFF, tid);
+        la.template load<sub>(a_ptr, A.ld, m0, k2);
+        lb.template load<sub>(b_ptr, B.ld, n0, k2);
+      } else if constexpr (sub == SUB - 2) {
+        static_for<2>([&](auto gg) EE_ALWAYS_INLINE {
+          constexpr int g = SUB - 2 + decltype(gg)::value;
+          la.template store<g>(next, tid);
+          lb.template store<g>(next + B_OFF, tid);
+          la.template load<g>(a_ptr, A.ld, m0, k2);
+          lb.template load<g>(b_ptr, B.ld, n0, k2);
+        });
+      }
       now.mma(acc);
-      // Interleave: one MFMA, then up to one of each memory kind.
       static_for<F::MMAS>([&](auto) EE_ALWAYS_INLINE {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
         __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
       });
+      if constexpr (sub == SUB - 2) __syncthreads();
     });
-    __syncthreads();
   }
 
   TileCtx<Cfg> t{s.M, s.N, m0, n0, tile_m, tile_n, wave_m, wave_n, lane, smem};
