@@ -3,11 +3,14 @@
 //
 // At decode the products are skinny, C[r][j] = sum_k W[r][k] Z[j][k] with
 // a weight W of R rows and only B <= 32 token rows Z per pass, so they are
-// bound by streaming W from HBM once.  One wave owns 32 rows of W and reads
-// them straight into MFMA A fragments (16 bytes of K per lane), 16
-// fragments in flight per lane per group of K, with no LDS; the token rows
-// come from L2 as B fragments (tokens past B re-read row B-1 and their
-// outputs are dropped).  bf16 uses v_mfma_f32_32x32x16_bf16, fp32
+// bound by streaming W from HBM once.  A block of four waves owns 32 rows of
+// W; each wave takes a quarter of K and reads its rows straight into MFMA A
+// fragments (16 bytes of K per lane), 8 fragments in flight per lane per
+// group, with no LDS staging; the token rows come from L2 as B fragments
+// (tokens past B re-read row B-1 and their outputs are dropped).  The four
+// partial sums meet in LDS in a fixed order and the first wave runs the
+// epilogue.  Splitting K gives about 4000 waves at V = 32000, enough loads in
+// flight on every CU.  bf16 uses v_mfma_f32_32x32x16_bf16, fp32
 // v_mfma_f32_32x32x2_f32 over the same 16-byte loads.
 //
 // Epilogues: store (gate projection), SwiGLU (up projection), residual
@@ -24,9 +27,10 @@ namespace ee {
 
 namespace {
 
-constexpr int kDecRows = 32;    // rows of W per wave (one block of 64 threads)
+constexpr int kDecRows = 32;    // rows of W per block
 constexpr int kDecTokens = 32;  // token rows per pass (grid.y walks more)
-constexpr int kDecGroup = 16;   // fragment loads per lane in flight
+constexpr int kDecWaves = 4;    // waves per block, each a quarter of K
+constexpr int kDecGroup = 8;    // fragment loads per operand per lane in flight
 
 template <typename T> struct DecFrag;
 // bf16: a 16-byte load holds 8 values of K; one MFMA consumes 16 (two lane halves).
@@ -55,12 +59,13 @@ __device__ __forceinline__ int dec_row(int r0, int lane, int v) {
 }
 
 template <typename T, class Epi>
-__global__ __launch_bounds__(64) void skinny_kernel(const T *__restrict__ W, int64_t ldw, int R,
-                                                    const T *__restrict__ Z, int64_t ldz, int B, int K,
-                                                    typename Epi::Params ep) {
+__global__ __launch_bounds__(64 * kDecWaves) void skinny_kernel(const T *__restrict__ W, int64_t ldw, int R,
+                                                                const T *__restrict__ Z, int64_t ldz, int B, int K,
+                                                                typename Epi::Params ep) {
   constexpr int KL = DecFrag<T>::K_PER_LOAD;
   constexpr int PER_LOAD = 16 / sizeof(T);  // elements of one 16-byte load
-  const int lane = threadIdx.x;
+  __shared__ f32x16_t red[kDecWaves - 1][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r0 = blockIdx.x * kDecRows, j0 = blockIdx.y * kDecTokens;
   const int wr = min(r0 + (lane & 31), R - 1);
   const int zr = min(j0 + (lane & 31), B - 1);
@@ -70,10 +75,15 @@ __global__ __launch_bounds__(64) void skinny_kernel(const T *__restrict__ W, int
   f32x16_t acc;
   static_for<16>([&](auto v) EE_ALWAYS_INLINE { acc[decltype(v)::value] = 0.0f; });
 
-  // Groups of kDecGroup loads (K multiple of the group's K), then groups of 4.
+  // This wave's share of K, in whole groups of 4 loads (K is a multiple of
+  // 4 KL): groups [g0, g1) of the K / (4 KL) groups.
+  constexpr int KG4 = 4 * KL;
+  const int groups = K / KG4;
+  const int g0 = wave * groups / kDecWaves, g1 = (wave + 1) * groups / kDecWaves;
+  int k = g0 * KG4;
+  const int kend = g1 * KG4;
   constexpr int KG = kDecGroup * KL;
-  int k = 0;
-  for (; k + KG <= K; k += KG) {
+  for (; k + KG <= kend; k += KG) {
     u32x4_t a[kDecGroup], b[kDecGroup];
     static_for<kDecGroup>([&](auto q) EE_ALWAYS_INLINE {
       constexpr int Q = decltype(q)::value;
@@ -85,8 +95,7 @@ __global__ __launch_bounds__(64) void skinny_kernel(const T *__restrict__ W, int
     __builtin_amdgcn_sched_barrier(0);
     static_for<kDecGroup>([&](auto q) EE_ALWAYS_INLINE { DecFrag<T>::mma(a[decltype(q)::value], b[decltype(q)::value], acc); });
   }
-  constexpr int KG4 = 4 * KL;
-  for (; k < K; k += KG4) {
+  for (; k < kend; k += KG4) {
     u32x4_t a[4], b[4];
     static_for<4>([&](auto q) EE_ALWAYS_INLINE {
       constexpr int Q = decltype(q)::value;
@@ -96,6 +105,12 @@ __global__ __launch_bounds__(64) void skinny_kernel(const T *__restrict__ W, int
     __builtin_amdgcn_sched_barrier(0);
     static_for<4>([&](auto q) EE_ALWAYS_INLINE { DecFrag<T>::mma(a[decltype(q)::value], b[decltype(q)::value], acc); });
   }
+  // Partial sums of waves 1..3 to LDS; wave 0 adds them in order and
+  // finishes.
+  if (wave > 0) red[wave - 1][lane] = acc;
+  __syncthreads();
+  if (wave != 0) return;
+  static_for<kDecWaves - 1>([&](auto w) EE_ALWAYS_INLINE { acc += red[decltype(w)::value][lane]; });
   Epi::apply(ep, acc, r0, j0, lane, R, B);
 }
 
@@ -292,8 +307,8 @@ hipError_t launch_skinny(const void *W, int64_t ldw, int R, const void *Z, int64
   if (K % (4 * DecFrag<T>::K_PER_LOAD) != 0) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>((R + kDecRows - 1) / kDecRows),
                   static_cast<unsigned>((B + kDecTokens - 1) / kDecTokens));
-  hipLaunchKernelGGL((skinny_kernel<T, Epi>), grid, dim3(64), 0, stream, static_cast<const T *>(W), ldw, R,
-                     static_cast<const T *>(Z), ldz, B, K, ep);
+  hipLaunchKernelGGL((skinny_kernel<T, Epi>), grid, dim3(64 * kDecWaves), 0, stream, static_cast<const T *>(W), ldw,
+                     R, static_cast<const T *>(Z), ldz, B, K, ep);
   return hipGetLastError();
 }
 
