@@ -206,7 +206,21 @@ __global__ __launch_bounds__(256) void ce_reduce_kernel(CeReduceArgs a) {
   const int n = blockIdx.x * 32 + tk;
   float m = -INFINITY, l = 0.0f;
   if (n < a.n) {
-    for (int t = tg; t < a.tiles; t += 8) {
+    // Tiles t = tg, tg + 8, ...: four rows' loads are issued before they are
+    // merged (in tile order), so the loop is not one load latency per tile.
+    int t = tg;
+    for (; t + 24 < a.tiles; t += 32) {
+      float pm[4], pl[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t o = static_cast<int64_t>(t + 8 * q) * a.ldn + n;
+        pm[q] = a.part_m[o];
+        pl[q] = a.part_l[o];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) lse_merge(m, l, pm[q], pl[q]);
+    }
+    for (; t < a.tiles; t += 8) {
       const int64_t o = static_cast<int64_t>(t) * a.ldn + n;
       lse_merge(m, l, a.part_m[o], a.part_l[o]);
     }
@@ -326,8 +340,21 @@ __global__ __launch_bounds__(256) void gain_reduce_kernel(const float *pa, int t
   const int j = blockIdx.x * 32 + c;
   float s = 0.0f;
   if (j < h) {
-    for (int t = g; t < ta; t += 8) s += pa[static_cast<int64_t>(t) * h + j];
-    for (int t = g; t < tb; t += 8) s += pb[static_cast<int64_t>(t) * h + j];
+    // Rows t = g, g + 8, ...: loads of four rows issued before their adds
+    // (in row order), so the loop is not one load latency per row.
+    auto sum_rows = [&](const float *p, int tiles) {
+      int t = g;
+      for (; t + 24 < tiles; t += 32) {
+        float v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = p[static_cast<int64_t>(t + 8 * q) * h + j];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s += v[q];
+      }
+      for (; t < tiles; t += 8) s += p[static_cast<int64_t>(t) * h + j];
+    };
+    sum_rows(pa, ta);
+    sum_rows(pb, tb);
   }
   red[g][c] = s;
   __syncthreads();
