@@ -94,7 +94,7 @@ typedef enum ee_norm { EE_NORM_RMS = 0, EE_NORM_LAYER = 1 } ee_norm;
 typedef struct ee_exit {
   int32_t kind;          /* ee_exit_kind                                     */
   int32_t dtype;         /* ee_dtype of the hidden states and all weights    */
-  int64_t hidden;        /* h: multiple of 64, 64 <= h <= 32768              */
+  int64_t hidden;        /* h: multiple of 64, 64 <= h <= 32768 (MLP: 8192)  */
   int64_t vocab;         /* V: 1 <= V <= 1048576                             */
   int64_t intermediate;  /* I (MLP only): multiple of 64, <= 65536; else 0   */
   float rms_eps;         /* norm epsilon, >= 0 (Llama-2 uses 1e-5)           */

@@ -32,6 +32,7 @@ constexpr int64_t kMaxTokens = 1 << 20;
 constexpr int64_t kMaxHidden = 32768;
 constexpr int64_t kMaxVocab = 1 << 20;
 constexpr int64_t kMaxInter = 65536;
+constexpr int64_t kMaxMlpHidden = 8192;  // the exit-norm backward keeps a row in registers
 constexpr size_t kAlign = 256;
 
 int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -46,6 +47,7 @@ struct Layout {
   size_t u = 0, uhat = 0, rx = 0, hg = 0, hu = 0, act = 0, y = 0, dz = 0, dy = 0, dhg = 0, dhu = 0,
          dgpg = 0, dgpu = 0;
   size_t mu = 0, gsp = 0, gsum = 0, dbp = 0;  // LayerNorm mean; bias: G row sums, bias partials
+  int dzs = 1;                                // split-K slices of the dZ product
   int64_t gchunks = 0;
   size_t total = 0;
 };
@@ -98,7 +100,8 @@ Layout layout(const ee_exit &e, int64_t n) {
     L.hu = take(N * I * es);
     L.act = take(N * I * es);
     L.y = take(N * h * 4);
-    L.dz = take(N * h * 4);
+    L.dzs = ee::dz_splits(f32, static_cast<int>(L.ldn), static_cast<int>(h), static_cast<int>(V));
+    L.dz = take(static_cast<size_t>(L.dzs) * N * h * 4);
     L.dy = take(N * h * es);
     L.dhg = take(N * I * es);
     L.dhu = take(N * I * es);
@@ -142,6 +145,8 @@ ee_status validate_exit(const ee_exit *e, int idx) {
     return fail(EE_ERR_SHAPE, "exit %d: vocab=%lld must be in [1, %lld]", idx, static_cast<long long>(e->vocab),
                 static_cast<long long>(kMaxVocab));
   if (e->kind == EE_EXIT_MLP) {
+    if (e->hidden > kMaxMlpHidden)
+      return fail(EE_ERR_SHAPE, "exit %d: an MLP exit needs hidden <= %lld", idx, static_cast<long long>(kMaxMlpHidden));
     if (e->intermediate < 64 || e->intermediate > kMaxInter || e->intermediate % 64 != 0)
       return fail(EE_ERR_SHAPE, "exit %d: intermediate=%lld must be a multiple of 64 in [64, %lld]", idx,
                   static_cast<long long>(e->intermediate), static_cast<long long>(kMaxInter));
@@ -361,8 +366,9 @@ ee_status run_backward(const ee_exit &e, int64_t n64, void *ws, const ee_exit_gr
   if (bias)
     EE_LAUNCH("exit bias gradient", s, ee::launch_gain_reduce(atf(ws, L.dbp), static_cast<int>(L.vtiles), nullptr, 0, h, g.d_beta, acc, s));
   if (e.kind != EE_EXIT_MLP) return EE_OK;
-  EE_LAUNCH("dZ", s, ee::gemm_dz(f32, at(ws, L.P), e.w_out, n, ldn, h, V, atf(ws, L.dz), s));
-  EE_LAUNCH("exit norm backward", s, ee::launch_norm_bwd(f32, atf(ws, L.dz), atf(ws, L.y), atf(ws, L.r), e.gamma, n, h, at(ws, L.dy), s));
+  EE_LAUNCH("dZ", s, ee::gemm_dz(f32, at(ws, L.P), e.w_out, n, ldn, h, V, atf(ws, L.dz), s, L.dzs));
+  EE_LAUNCH("exit norm backward", s, ee::launch_norm_bwd(f32, atf(ws, L.dz), atf(ws, L.y), atf(ws, L.r), e.gamma, n, h, at(ws, L.dy), s,
+                                                         L.dzs, static_cast<int64_t>(n) * h));
   EE_LAUNCH("dA + swiglu backward", s, ee::gemm_da_swiglu(f32, at(ws, L.dy), e.w_down, n, I, h, at(ws, L.hg), at(ws, L.hu), at(ws, L.dhg),
                             at(ws, L.dhu), s));
   EE_LAUNCH("down gradient", s, ee::gemm_dw_down(f32, at(ws, L.dy), at(ws, L.act), n, h, I, g.d_w_down, acc, s));

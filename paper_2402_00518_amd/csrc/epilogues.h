@@ -240,7 +240,8 @@ struct EpiWeightGrad {
 };
 
 // fp32 store with optional accumulation (dW += C).  Rows at or beyond
-// `rows` are not stored (the GEMM may run over padding).
+// `rows` are not stored (the GEMM may run over padding).  With split K,
+// slice z of the product goes to C + z * zstride (partial sums).
 template <typename T>
 struct EpiStoreF32 {
   struct Params {
@@ -248,9 +249,12 @@ struct EpiStoreF32 {
     int64_t ldc;
     int rows;
     int accumulate;
+    int64_t zstride;
   };
   template <class Cfg>
-  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+  __device__ __forceinline__ static void apply(const Params &p0, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    Params p = p0;
+    p.C += t.kz * p.zstride;
     with_flag(p.accumulate != 0, [&](auto A_) EE_ALWAYS_INLINE {
       if constexpr (!decltype(A_)::value) {
         for_each_acc<Cfg>(acc, t, [&](int row, int col, int, float a) EE_ALWAYS_INLINE {

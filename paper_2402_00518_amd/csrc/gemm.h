@@ -4,10 +4,11 @@
 //
 // Each operand is either K-major (element (r, k) at ptr[r*ld + k], K
 // contiguous) or MN-major (element (r, k) at ptr[k*ld + r], rows
-// contiguous).  Tiles are staged through LDS in one canonical K-contiguous
-// layout, so the MFMA fragment reads are the same for both: an MN-major
-// operand is transposed in registers (4 k-rows x one 16-byte column group
-// per thread) on its way into LDS.
+// contiguous).  K-major tiles sit in LDS as rows of K; bf16 MN-major tiles
+// are copied as they are (k-rows) and transposed by the fragment reads
+// themselves (ds_read_b64_tr_b16), so neither side spends ALU work on the
+// layout.  (fp32 MN-major operands, used only by the fp32 path, are
+// transposed in registers on their way into LDS.)
 //
 // A tile configuration fixes the output tile (BM x BN) and the part of it
 // each wave64 owns (WM x WN = MB x NB blocks of 32 x 32 accumulators).  Each
@@ -36,6 +37,7 @@ struct Operand {
 
 struct GemmShape {
   int M, N, K;
+  int kchunk = 0;  // split-K: blockIdx.z covers K values [z kchunk, (z + 1) kchunk); 0 = all of K
 };
 
 constexpr int kRowBytes = 128;
@@ -77,23 +79,15 @@ template <> struct Elem<float> {
 
 __host__ __device__ constexpr int cdiv(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
 
-// Byte offset of 16-byte chunk `ch` (0..7) of LDS tile row `row`.  A
-// ds_read_b128 is served 16 lanes at a time from 256 bytes of banks, i.e.
+// Byte offset of 16-byte chunk `ch` (0..7) of K-major LDS tile row `row`.
+// A ds_read_b128 is served 16 lanes at a time from 256 bytes of banks, i.e.
 // two 128-byte tile rows; the 16 lanes of a fragment read read 16
 // consecutive rows at one logical chunk, so within every aligned group of 16
-// rows, rows of equal parity must land on distinct chunks: the XOR key's
-// bits come from row / 2.  That key repeats every 16 rows, so a lane's
-// fragment rows 32 apart share one swizzle and their addresses differ by a
-// constant.  Tiles written by the MN-major bf16 loader, whose lanes write
-// rows 8 apart, fold row / 16 into the key as well (WIDE), which spreads
-// those writes over all chunks.
-template <bool WIDE>
-__device__ __forceinline__ int lds_key(int row) {
-  return WIDE ? ((row >> 1) ^ (row >> 4)) & 7 : (row >> 1) & 7;
-}
-template <bool WIDE = false>
+// rows, rows of equal parity must land on distinct chunks: the XOR key is
+// (row / 2) mod 8.  It repeats every 16 rows, so a lane's fragment rows 32
+// apart share one swizzle and their addresses differ by a constant.
 __device__ __forceinline__ int lds_off(int row, int ch) {
-  return row * kRowBytes + ((ch ^ lds_key<WIDE>(row)) << 4);
+  return row * kRowBytes + ((ch ^ ((row >> 1) & 7)) << 4);
 }
 
 // ---------------------------------------------------------------- loaders
@@ -165,95 +159,67 @@ struct MNMajorLoaderGrouped : MNMajorLoader<T, ROWS, THREADS> {
   }
 };
 
-// bf16, 64 k-rows x ROWS operand rows per stage, in blocks of 4 k-rows x 8
-// operand rows (one 16-byte load per k-row), one block per thread.  Inside
-// a wave, lane bits 0-2 pick 8 consecutive column groups (128 contiguous
-// bytes of one k-row per load) and bits 3-5 pick the k-block, so each load
-// instruction reads whole 128-byte lines.  A block becomes 8 LDS rows of 4 k
-// values (8 bytes); each ds_write_b64 writes the even rows of half the lanes
-// and the odd rows of the other half, which with the WIDE lds_key reaches
-// every bank.
-// The byte shuffles are v_perm_b32, whose per-lane selector also makes that
-// even/odd choice.  The whole stage is loaded and written in the first
-// substep: the writes need all four k-rows of a block, and loading them at
-// once gives each a full stage of latency.
-// K-rows past the end re-read the last k-row; with ZERO_TAIL they are
-// written to LDS as zeros.  One operand of a product zeroed is enough, so
-// only the A side pays for it.
+// bf16 MN-major tile, stored in LDS as it is in memory: 64 k-rows of ROWS
+// operand rows (2 ROWS bytes each), 16-byte chunks XOR-swizzled by
+// 4 (k mod 4) (see mn_off).  The transpose happens in the fragment reads
+// (ds_read_b64_tr_b16, see Frags), so the copy is a plain one: each thread
+// moves PER 16-byte chunks, one per substep group, consecutive threads
+// along a k-row (whole 128-byte lines per load).  K-rows past the end
+// re-read the last k-row; with ZERO_TAIL they are written as zeros.  One
+// operand of a product zeroed is enough, so only the A side pays for it.
+template <int ROWS>
+__device__ __forceinline__ int mn_off(int k, int m) {
+  return k * (2 * ROWS) + (((m >> 3) ^ (4 * (k & 3))) << 4) + (m & 7) * 2;
+}
+
 template <int ROWS, int THREADS, int GROUPS, bool ZERO_TAIL>
 struct MNMajorLoaderB16 {
-  static constexpr int MBW = ROWS / 64;  // 8-block column groups per tile
-  static_assert(16 * ROWS / 8 == THREADS, "one 4 x 8 block per thread");
-  u32x4_t reg[4];   // k-rows 0..3 of the block
-  uint32_t goff;    // byte offset of the block's first k-row in a stage's panel
-  int kr0;          // first k-row of the block inside the stage
-  int lim;          // last valid k-row of the block (relative), as of the last load
+  static constexpr int CHUNKS = ROWS / 8;               // 16-byte chunks per k-row
+  static constexpr int PER = 64 * CHUNKS / THREADS;     // chunks per thread per stage
+  static constexpr int PG = PER / GROUPS;
+  static_assert(PER % GROUPS == 0 && CHUNKS >= 16, "stage chunks must split evenly; swizzle needs 16 chunks");
+  u32x4_t reg[PER];
+  uint32_t moff[PER];   // byte offset of the chunk's operand row within a k-row (clamped)
+  int kr[PER];          // k-row of the chunk inside the stage
+  int loff[PER];        // LDS byte offset of the chunk
   int K_;
-  int lbase;        // LDS byte offset of the block's first row (with the even/odd choice)
-  int c0;           // logical chunk XOR the rows' swizzle key (before the row pair index)
-  uint32_t sel_first;  // v_perm_b32 selector of the row written first
-  int dsec;             // byte distance from the first row written to the second
+  int lim;              // K - 1 - k0 of the last load (k-rows beyond it are past K)
 
-  __device__ __forceinline__ void init(int64_t ld, int row0, int rows, int K, int tid) {
-    const int lane = tid & 63, wb = tid >> 6;
-    const int mb = (lane & 7) + 8 * (wb % MBW);
-    const int kb = (lane >> 3) + 8 * (wb / MBW);
-    const int mcol = min(row0 + mb * 8, rows - 8) - row0;  // rows is a multiple of 8
-    kr0 = kb * 4;
-    goff = static_cast<uint32_t>((static_cast<int64_t>(kr0) * ld + mcol) * 2);
+  __device__ __forceinline__ void init(int64_t, int row0, int rows, int K, int tid) {
     K_ = K;
-    lim = 3;
-    const int sw = (lane >> 5) & 1;  // this lane writes the odd row of each pair first
-    // rows mb*8 + 2j + {0, 1} share lds_key = K0 ^ j (j < 4)
-    const int key0 = ((4 * (mb & 1)) ^ ((mb >> 1) & 7)) & 7;
-    c0 = (kb >> 1) ^ key0;
-    lbase = mb * 8 * kRowBytes + sw * kRowBytes + (kb & 1) * 8;
-    // v_perm_b32(x = k-row pair high, y = k-row pair low): even operand row
-    // takes the low 16 bits of both, odd operand row the high 16 bits.
-    sel_first = sw ? 0x07060302u : 0x05040100u;
-    dsec = sw ? -kRowBytes : kRowBytes;
+    lim = 63;
+    static_for<PER>([&](auto i) EE_ALWAYS_INLINE {
+      const int c = tid + decltype(i)::value * THREADS;
+      const int k = c / CHUNKS, ch = c % CHUNKS;
+      const int m = min(row0 + ch * 8, rows - 8) - row0;  // rows is a multiple of 8
+      kr[i] = k;
+      moff[i] = static_cast<uint32_t>(m * 2);
+      loff[i] = k * (2 * ROWS) + ((ch ^ (4 * (k & 3))) << 4);
+    });
   }
   template <int G>
   __device__ __forceinline__ void load(const bf16_t *base, int64_t ld, int row0, int k0) {
-    if constexpr (G == 0) {
-      const char *panel = reinterpret_cast<const char *>(base + static_cast<int64_t>(k0) * ld + row0);
-      const int l = min(3, K_ - 1 - k0 - kr0);  // k-rows past K re-read the last one
-      // l < 0 when the whole block lies past K: the (negative) row offset
-      // then points back at k-row K - 1, and goff + offset stays >= 0.
-      const int ld2 = static_cast<int>(ld * 2);  // < 2^23, checked by the launcher
-      static_for<4>([&](auto r) EE_ALWAYS_INLINE {
-        const int rr = min(static_cast<int>(decltype(r)::value), l);
-        reg[r] = *reinterpret_cast<const u32x4_t *>(panel + (goff + static_cast<uint32_t>(__mul24(rr, ld2))));
-      });
-      if constexpr (ZERO_TAIL) lim = l;
-    }
+    const char *panel = reinterpret_cast<const char *>(base + static_cast<int64_t>(k0) * ld + row0);
+    const int l = K_ - 1 - k0;
+    const int ld2 = static_cast<int>(ld * 2);  // < 2^23, checked by the launcher
+    static_for<PG>([&](auto q) EE_ALWAYS_INLINE {
+      constexpr int i = G * PG + decltype(q)::value;
+      const int k = min(kr[i], l);
+      reg[i] = *reinterpret_cast<const u32x4_t *>(panel + (moff[i] + static_cast<uint32_t>(__mul24(k, ld2))));
+    });
+    if constexpr (ZERO_TAIL && G == GROUPS - 1) lim = l;
   }
   template <int G>
   __device__ __forceinline__ void store(char *lds, int) const {
-    if constexpr (G == 0) {
-      u32x4_t a[4];
-      static_for<4>([&](auto r) EE_ALWAYS_INLINE {
-        constexpr int R = decltype(r)::value;
-        if constexpr (ZERO_TAIL) {
-          const bool ok = R <= lim;
-          static_for<4>([&](auto j) EE_ALWAYS_INLINE { a[R][decltype(j)::value] = ok ? reg[R][decltype(j)::value] : 0u; });
-        } else {
-          a[R] = reg[R];
-        }
-      });
-      static_for<4>([&](auto jj) EE_ALWAYS_INLINE {
-        constexpr int j = decltype(jj)::value;
-        // dword j of a k-row holds operand rows 2j (low half) and 2j+1 (high half)
-        const uint32_t sel_second = sel_first ^ 0x02020202u;  // the other half of each dword
-        const u32x2_t first = {__builtin_amdgcn_perm(a[1][j], a[0][j], sel_first),
-                               __builtin_amdgcn_perm(a[3][j], a[2][j], sel_first)};
-        const u32x2_t second = {__builtin_amdgcn_perm(a[1][j], a[0][j], sel_second),
-                                __builtin_amdgcn_perm(a[3][j], a[2][j], sel_second)};
-        const int off = lbase + j * 2 * kRowBytes + ((c0 ^ j) << 4);
-        *reinterpret_cast<u32x2_t *>(lds + off) = first;
-        *reinterpret_cast<u32x2_t *>(lds + off + dsec) = second;
-      });
-    }
+    static_for<PG>([&](auto q) EE_ALWAYS_INLINE {
+      constexpr int i = G * PG + decltype(q)::value;
+      u32x4_t v = reg[i];
+      if constexpr (ZERO_TAIL) {
+        const bool ok = kr[i] <= lim;
+        static_for<4>([&](auto j) EE_ALWAYS_INLINE { v[decltype(j)::value] = ok ? v[decltype(j)::value] : 0u; });
+      }
+      *reinterpret_cast<u32x4_t *>(lds + loff[i]) = v;
+    });
   }
 };
 
@@ -305,23 +271,63 @@ template <int ROWS, int THREADS, int GROUPS, bool ZERO_TAIL> struct LoaderSel<bf
 // ------------------------------------------------------------ MFMA step
 // Fragments of one K substep (16 values of K) for the wave's MB x NB blocks
 // of 32 x 32, read from one LDS stage, and the MFMAs that consume them.
-template <typename T, class Cfg, bool A_WIDE, bool B_WIDE> struct Frags;
+template <typename T, class Cfg, bool A_MN, bool B_MN> struct Frags;
 
-template <class Cfg, bool A_WIDE, bool B_WIDE> struct Frags<bf16_t, Cfg, A_WIDE, B_WIDE> {
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+
+// Lane base offsets of the MFMA fragment reads of one operand of a wave:
+// `blocks` blocks of 32 rows from row0.  K-major tiles: row (row0 + 32 b +
+// lane % 32), logical chunk (lane / 32) (the substep adds 2 chunks).
+// MN-major tiles (k-rows of ROWS operand rows): ds_read_b64_tr_b16 gives
+// lane 4a + b of each 16-lane group element b of the 8-byte chunks that
+// lanes a, a + 4, a + 8, a + 12 of the group address.  Lane j of group g
+// therefore addresses k-row 8 (g / 2) + j / 4 (+ 4 for the second read,
+// + 16 per substep) at operand rows m0 + 16 (g % 2) + 4 (j % 4) .. + 3, and
+// receives rows m0 + 16 (g % 2) + j at four consecutive k: with the second
+// read, the 8 values of K that the MFMA expects of lane (row = lane % 32,
+// k = 8 (lane / 32) + e).  K offsets that are multiples of 4 keep the
+// swizzle (4 (k mod 4)), so they go into the instruction offset.
+template <bool MN, int ROWS>
+__device__ __forceinline__ int frag_base(int row0, int lane) {
+  if constexpr (MN) {
+    const int g = lane >> 4, j = lane & 15;
+    return mn_off<ROWS>(8 * (g >> 1) + (j >> 2), row0 + 16 * (g & 1) + 4 * (j & 3));
+  } else {
+    return 0;  // unused: K-major reads compute lds_off directly
+  }
+}
+
+template <class Cfg, bool A_MN, bool B_MN> struct Frags<bf16_t, Cfg, A_MN, B_MN> {
   static constexpr int MB = Cfg::MB, NB = Cfg::NB;
   static constexpr int SUBSTEPS = 4;  // 4 x 16 = 64 values of K per stage
   static constexpr int MMAS = MB * NB;  // MFMAs per substep
   bf16x8_t a[MB], b[NB];
 
-  __device__ __forceinline__ void load(const char *a_lds, const char *b_lds, int a_row0, int b_row0,
-                                       int lane, int s) {
-    const int r = lane & 31, ch = s * 2 + (lane >> 5);
-    static_for<MB>([&](auto i) EE_ALWAYS_INLINE {
-      a[i] = *reinterpret_cast<const bf16x8_t *>(a_lds + lds_off<A_WIDE>(a_row0 + i * 32 + r, ch));
-    });
-    static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
-      b[j] = *reinterpret_cast<const bf16x8_t *>(b_lds + lds_off<B_WIDE>(b_row0 + j * 32 + r, ch));
-    });
+  // One operand's fragments of substep s.  `base` = frag_base of each block
+  // (MN-major tiles), or the tile's first row (K-major tiles).
+  template <bool MN, int ROWS, int NBLK>
+  __device__ __forceinline__ static void read(bf16x8_t (&f)[NBLK], const char *lds, const int (&base)[NBLK],
+                                              int row0, int lane, int s) {
+    if constexpr (MN) {
+      static_for<NBLK>([&](auto i) EE_ALWAYS_INLINE {
+        const char *p = lds + base[i] + 16 * s * (2 * ROWS);
+        const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)(p));
+        const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)(p + 4 * (2 * ROWS)));
+        const s16x4_t both[2] = {lo, hi};
+        f[i] = __builtin_bit_cast(bf16x8_t, both);
+      });
+    } else {
+      const int r = lane & 31, ch = s * 2 + (lane >> 5);
+      static_for<NBLK>([&](auto i) EE_ALWAYS_INLINE {
+        f[i] = *reinterpret_cast<const bf16x8_t *>(lds + lds_off(row0 + i * 32 + r, ch));
+      });
+    }
+  }
+  __device__ __forceinline__ void load(const char *a_lds, const char *b_lds, const int (&a_base)[MB],
+                                       const int (&b_base)[NB], int a_row0, int b_row0, int lane, int s) {
+    read<A_MN, Cfg::BM>(a, a_lds, a_base, a_row0, lane, s);
+    read<B_MN, Cfg::BN>(b, b_lds, b_base, b_row0, lane, s);
   }
   __device__ __forceinline__ void mma(f32x16_t (&acc)[MB][NB]) const {
     static_for<MB>([&](auto i) EE_ALWAYS_INLINE {
@@ -332,15 +338,16 @@ template <class Cfg, bool A_WIDE, bool B_WIDE> struct Frags<bf16_t, Cfg, A_WIDE,
   }
 };
 
-template <class Cfg, bool A_WIDE, bool B_WIDE> struct Frags<float, Cfg, A_WIDE, B_WIDE> {
-  static_assert(!A_WIDE && !B_WIDE, "fp32 tiles use the narrow swizzle");
+template <class Cfg, bool A_MN, bool B_MN> struct Frags<float, Cfg, A_MN, B_MN> {
+  // fp32 MN-major operands are transposed in registers on their way into
+  // LDS, so both fp32 operands are read K-major here.
   static constexpr int MB = Cfg::MB, NB = Cfg::NB;
   static constexpr int SUBSTEPS = 2;  // 2 x 16 = 32 values of K per stage
   static constexpr int MMAS = 8 * MB * NB;  // MFMAs per substep
   f32x4_t a[MB][2], b[NB][2];
 
-  __device__ __forceinline__ void load(const char *a_lds, const char *b_lds, int a_row0, int b_row0,
-                                       int lane, int s) {
+  __device__ __forceinline__ void load(const char *a_lds, const char *b_lds, const int (&)[MB], const int (&)[NB],
+                                       int a_row0, int b_row0, int lane, int s) {
     const int r = lane & 31, half = lane >> 5;
     static_for<2>([&](auto c) EE_ALWAYS_INLINE {
       const int ch = s * 4 + half * 2 + c;
@@ -376,6 +383,7 @@ struct TileCtx {
   int tile_m, tile_n;  // tile indices
   int wave_m, wave_n, lane;
   char *smem;          // LDS free for the epilogue (>= WAVES_M * BN floats)
+  int kz = 0;          // split-K slice of this block (epilogues that support splits offset by it)
 
   __device__ __forceinline__ int row(int i, int v) const {
     return m0 + wave_m * Cfg::WM + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
@@ -439,7 +447,8 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
   const T *b_ptr = static_cast<const T *>(B.ptr);
 
   constexpr bool kB16 = std::is_same<T, bf16_t>::value;
-  using F = Frags<T, Cfg, kB16 && !AK, kB16 && !BKM>;
+  constexpr bool kAMN = kB16 && !AK, kBMN = kB16 && !BKM;  // read with the LDS transpose
+  using F = Frags<T, Cfg, kAMN, kBMN>;
   constexpr int SUB = F::SUBSTEPS;
   typename LoaderSel<T, AK, Cfg::BM, Cfg::THREADS, SUB, true>::type la;
   typename LoaderSel<T, BKM, Cfg::BN, Cfg::THREADS, SUB, false>::type lb;
@@ -467,36 +476,42 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
   // for LDS.  The code of a stage has no branches (loads past the last
   // stage re-read it), so the scheduler sees each stage as one region.
   constexpr int B_OFF = Cfg::BM * kRowBytes;
-  const int nk = cdiv(s.K, BK);
+  const int kz = blockIdx.z;
+  const int kbeg = s.kchunk > 0 ? kz * s.kchunk : 0;
+  const int kend = s.kchunk > 0 ? min(s.K, kbeg + s.kchunk) : s.K;
+  const int nk = cdiv(kend - kbeg, BK);
   const int a_row0 = wave_m * Cfg::WM, b_row0 = wave_n * Cfg::WN;
   static_for<SUB>([&](auto g) EE_ALWAYS_INLINE {
-    la.template load<decltype(g)::value>(a_ptr, A.ld, m0, 0);
-    lb.template load<decltype(g)::value>(b_ptr, B.ld, n0, 0);
+    la.template load<decltype(g)::value>(a_ptr, A.ld, m0, kbeg);
+    lb.template load<decltype(g)::value>(b_ptr, B.ld, n0, kbeg);
   });
   static_for<SUB>([&](auto g) EE_ALWAYS_INLINE {
     la.template store<decltype(g)::value>(smem, tid);
     lb.template store<decltype(g)::value>(smem + B_OFF, tid);
   });
-  const int k1 = min(1, nk - 1) * BK;
+  const int k1 = kbeg + min(1, nk - 1) * BK;
   static_for<SUB>([&](auto g) EE_ALWAYS_INLINE {
     la.template load<decltype(g)::value>(a_ptr, A.ld, m0, k1);
     lb.template load<decltype(g)::value>(b_ptr, B.ld, n0, k1);
   });
   __syncthreads();
+  int a_base[MB], b_base[NB];
+  static_for<MB>([&](auto i) EE_ALWAYS_INLINE { a_base[i] = frag_base<kAMN, Cfg::BM>(a_row0 + 32 * i, lane); });
+  static_for<NB>([&](auto j) EE_ALWAYS_INLINE { b_base[j] = frag_base<kBMN, Cfg::BN>(b_row0 + 32 * j, lane); });
   F f0, f1;
-  f0.load(smem, smem + B_OFF, a_row0, b_row0, lane, 0);
+  f0.load(smem, smem + B_OFF, a_base, b_base, a_row0, b_row0, lane, 0);
   for (int kt = 0; kt < nk; ++kt) {
     const char *cur = smem + (kt & 1) * Cfg::STAGE_BYTES;
     char *next = smem + ((kt + 1) & 1) * Cfg::STAGE_BYTES;
-    const int k2 = min(kt + 2, nk - 1) * BK;
+    const int k2 = kbeg + min(kt + 2, nk - 1) * BK;
     static_for<SUB>([&](auto st) EE_ALWAYS_INLINE {
       constexpr int sub = decltype(st)::value;
       F &now = (sub % 2 == 0) ? f0 : f1;
       F &later = (sub % 2 == 0) ? f1 : f0;
       if constexpr (sub + 1 < SUB)
-        later.load(cur, cur + B_OFF, a_row0, b_row0, lane, sub + 1);
+        later.load(cur, cur + B_OFF, a_base, b_base, a_row0, b_row0, lane, sub + 1);
       else
-        later.load(next, next + B_OFF, a_row0, b_row0, lane, 0);  // next stage, published by the barrier
+        later.load(next, next + B_OFF, a_base, b_base, a_row0, b_row0, lane, 0);  // next stage, published by the barrier
       if constexpr (sub < SUB - 2) {
         la.template store<sub>(next, tid);
         lb.template store<sub>(next + B_OFF, tid);
@@ -522,7 +537,7 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
     });
   }
 
-  TileCtx<Cfg> t{s.M, s.N, m0, n0, tile_m, tile_n, wave_m, wave_n, lane, smem};
+  TileCtx<Cfg> t{s.M, s.N, m0, n0, tile_m, tile_n, wave_m, wave_n, lane, smem, kz};
   Epi::template apply<Cfg>(ep, acc, t);
 }
 
@@ -536,7 +551,12 @@ hipError_t launch_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Pa
     return hipErrorInvalidValue;  // shapes the loaders do not handle
   if ((!AK && A.ld >= (int64_t{1} << 22)) || (!BKM && B.ld >= (int64_t{1} << 22)))
     return hipErrorInvalidValue;  // MN-major loaders keep signed 24-bit k-row strides
-  hipLaunchKernelGGL((gemm_kernel<T, AK, BKM, Epi, Cfg>), dim3(static_cast<unsigned>(blocks)),
+  int splits = 1;
+  if (s.kchunk > 0) {
+    if (s.kchunk % BK != 0) return hipErrorInvalidValue;  // slices start on stage boundaries
+    splits = cdiv(s.K, s.kchunk);
+  }
+  hipLaunchKernelGGL((gemm_kernel<T, AK, BKM, Epi, Cfg>), dim3(static_cast<unsigned>(blocks), 1, splits),
                      dim3(Cfg::THREADS), 0, stream, A, B, s, ep);
   return hipGetLastError();
 }

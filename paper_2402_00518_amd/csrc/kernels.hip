@@ -162,31 +162,58 @@ __global__ __launch_bounds__(256) void norm_apply_kernel(const Tin *x, int64_t l
 }
 
 // RMSNorm backward, one wave per row (see launch.h for the formula).
-template <typename T>
-__global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, const float *y, const float *r,
-                                                       const T *gain, int n, int h, T *dy) {
+constexpr int kNormBwdMaxH = 16 * kWave * 8;  // 8192: at most 16 8-wide chunks per lane
+
+// dZ arrives as `splits` partial sums zstride apart (split-K GEMM), added
+// here in slice order.
+__device__ __forceinline__ void load_dz8(const float *dz, int64_t o, int splits, int64_t zstride, float (&a)[8]) {
+  load_f32<8>(dz + o, a);
+  for (int z = 1; z < splits; ++z) {
+    float t[8];
+    load_f32<8>(dz + z * zstride + o, t);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) a[e] += t[e];
+  }
+}
+
+template <typename T, int CH>
+__global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int splits, int64_t zstride, const float *y,
+                                                       const float *r, const T *gain, int n, int h, T *dy) {
+  // One wave per row; the row's dZ * gain stays in registers (CH 8-wide
+  // chunks per lane, h <= CH * 512) between the projection and the output,
+  // so dZ's slices are read once.
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= n) return;
   const int64_t o = static_cast<int64_t>(row) * h;
   const float rr = r[row];
+  float dg[CH][8];
   float s = 0.0f;
-  for (int j = lane * 8; j < h; j += kWave * 8) {
-    float a[8], b[8], g[8];
-    load_f32<8>(dz + o + j, a);
-    load_f32<8>(y + o + j, b);
-    load_f32<8>(gain + j, g);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s += a[e] * g[e] * b[e] * rr;
+  for (int c = 0; c < CH; ++c) {
+    const int j = (c * kWave + lane) * 8;
+    if (j < h) {
+      float g[8], yy[8];
+      load_dz8(dz, o + j, splits, zstride, dg[c]);
+      load_f32<8>(y + o + j, yy);
+      load_f32<8>(gain + j, g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        dg[c][e] *= g[e];
+        s += dg[c][e] * yy[e] * rr;
+      }
+    }
   }
   const float proj = warp_sum(s) / static_cast<float>(h);
-  for (int j = lane * 8; j < h; j += kWave * 8) {
-    float a[8], b[8], g[8], d[8];
-    load_f32<8>(dz + o + j, a);
-    load_f32<8>(y + o + j, b);
-    load_f32<8>(gain + j, g);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) d[e] = rr * (a[e] * g[e] - b[e] * rr * proj);
-    store_f32<8>(dy + o + j, d);
+  for (int c = 0; c < CH; ++c) {
+    const int j = (c * kWave + lane) * 8;
+    if (j < h) {
+      float yy[8], d[8];
+      load_f32<8>(y + o + j, yy);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = rr * (dg[c][e] - yy[e] * rr * proj);
+      store_f32<8>(dy + o + j, d);
+    }
   }
 }
 
@@ -440,9 +467,21 @@ hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *par
 }
 
 hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const float *r, const void *gain, int n,
-                           int h, void *dy, hipStream_t stream) {
-  EE_DISPATCH(f32, hipLaunchKernelGGL(norm_bwd_kernel<T>, dim3(cdiv(n, 4)), dim3(256), 0, stream, dz, y, r,
-                                      static_cast<const T *>(gain), n, h, static_cast<T *>(dy)));
+                           int h, void *dy, hipStream_t stream, int splits, int64_t zstride) {
+  if (h > kNormBwdMaxH) return hipErrorInvalidValue;
+  const dim3 grid(cdiv(n, 4));
+  EE_DISPATCH(f32, {
+    const T *g = static_cast<const T *>(gain);
+    T *d = static_cast<T *>(dy);
+    if (h <= 2048)
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 4>), grid, dim3(256), 0, stream, dz, splits, zstride, y, r, g, n, h, d);
+    else if (h <= 4096)
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 8>), grid, dim3(256), 0, stream, dz, splits, zstride, y, r, g, n, h, d);
+    else if (h <= 6144)
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 12>), grid, dim3(256), 0, stream, dz, splits, zstride, y, r, g, n, h, d);
+    else
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 16>), grid, dim3(256), 0, stream, dz, splits, zstride, y, r, g, n, h, d);
+  });
   return hipGetLastError();
 }
 
@@ -533,12 +572,26 @@ hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, con
   return hipSuccess;
 }
 
+int dz_splits(bool f32, int ldn, int h, int vocab) {
+  // Split K until the product has about four rounds of tiles on the GPU's
+  // 256 CUs (a shape-only rule, so results do not depend on the device):
+  // at most 4 slices, each at least 4 stages deep.
+  if (f32) return 1;
+  const int tiles = cdiv(ldn, CfgBig::BM) * cdiv(h, CfgBig::BN);
+  int s = 1;
+  while (s < 4 && tiles * s < 1024 && vocab / (2 * s) >= 4 * 64) s *= 2;
+  return cdiv(vocab, dz_kchunk(vocab, s));
+}
+
+int dz_kchunk(int vocab, int splits) { return cdiv(cdiv(vocab, splits), 64) * 64; }
+
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab, float *dz,
-                   hipStream_t stream) {
+                   hipStream_t stream, int splits) {
   EE_DISPATCH(f32, {
-    typename EpiStoreF32<T>::Params ep{dz, h, n, 0};
-    return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{g_t, ldn}, Operand{w_out, h},
-                                                        GemmShape{ldn, h, vocab}, ep, stream);
+    typename EpiStoreF32<T>::Params ep{dz, h, n, 0, static_cast<int64_t>(n) * h};
+    GemmShape sh{ldn, h, vocab};
+    if (splits > 1) sh.kchunk = dz_kchunk(vocab, splits);
+    return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{g_t, ldn}, Operand{w_out, h}, sh, ep, stream);
   });
   return hipSuccess;
 }

@@ -66,9 +66,10 @@ hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *par
                               int h, float *out, int accumulate, hipStream_t stream);
 
 // RMSNorm backward through the exit norm of an MLP exit:
-//   dz_hat = dZ * gain,  z_hat = y * r,  dY = r (dz_hat - z_hat mean_j(dz_hat z_hat)).
+//   dz_hat = dZ * gain,  z_hat = y * r,  dY = r (dz_hat - z_hat mean_j(dz_hat z_hat)),
+// with dZ the sum of `splits` partial products zstride floats apart.
 hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const float *r, const void *gain,
-                           int n, int h, void *dy, hipStream_t stream);
+                           int n, int h, void *dy, hipStream_t stream, int splits = 1, int64_t zstride = 0);
 
 hipError_t launch_clear_flag(int *flag, hipStream_t stream);
 
@@ -97,9 +98,13 @@ hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int 
 // Y[n][h] = X + A W_down^T  (fp32 out).
 hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, const void *x, int n,
                               int h, int inter, float *y, hipStream_t stream);
-// dZ[n][h] = G W_out with G stored transposed [V][ldn]  (fp32 out).
+// dZ[n][h] = G W_out with G stored transposed [V][ldn]  (fp32 out), as
+// `splits` partial sums over slices of the vocabulary, n*h floats apart
+// (dz_splits: the count for a shape; the buffer holds that many slices).
+int dz_splits(bool f32, int ldn, int h, int vocab);
+int dz_kchunk(int vocab, int splits);
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab,
-                   float *dz, hipStream_t stream);
+                   float *dz, hipStream_t stream, int splits = 1);
 // dA = dY W_down with the SwiGLU backward epilogue.
 hipError_t gemm_da_swiglu(bool f32, const void *dy, const void *w_down, int n, int inter, int h,
                           const void *hg, const void *hu, void *dhg, void *dhu, hipStream_t stream);

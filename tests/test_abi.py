@@ -332,3 +332,8 @@ def test_decide_rejects_bad_arguments():
     assert decide_status(e, ws=0x10_0000_0000) == B.EE_ERR_ALIAS             # workspace over W_out
     bad = fake_exit(); bad.kind = B.EE_EXIT_LAYER
     assert decide_status(bad) == B.EE_ERR_UNSUPPORTED
+
+
+def test_mlp_exit_hidden_limit():
+    e = fake_exit(B.EE_EXIT_MLP, h=8256, I=512)
+    expect(fwd(e), B.EE_ERR_SHAPE, "MLP exit needs hidden")
