@@ -62,8 +62,8 @@ Layout layout(const ee_exit &e, int64_t n) {
   const size_t I = static_cast<size_t>(e.intermediate), N = static_cast<size_t>(n);
   L.ldn = cdiv64(n, ee::kTokenPad) * ee::kTokenPad;
   const bool f32 = e.dtype == EE_F32;
-  L.vtile = ee::gemm_tile_rows(f32, true, true);     // logits and dW_out GEMMs
-  L.itile = ee::gemm_tile_rows(f32, false, false);   // dW_gate / dW_up GEMMs
+  L.vtile = ee::gemm_part_cols(f32);  // partial slices of the logits and dW_out GEMMs
+  L.itile = ee::gemm_part_cols(f32);  // and of the dW_gate / dW_up GEMMs
   L.vtiles = cdiv64(e.vocab, L.vtile);
   L.itiles = cdiv64(e.intermediate, L.itile);
   const size_t ldn = static_cast<size_t>(L.ldn);

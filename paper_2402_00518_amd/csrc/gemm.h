@@ -416,18 +416,25 @@ __device__ __forceinline__ void tile_col_reduce(const TileCtx<Cfg> &t, float (&p
   __syncthreads();
 }
 
-// Logical tile of this block (XCD-aware, GROUP_M-grouped order).
+// Logical tile of this block (XCD-aware, grouped order).  Blocks that run
+// together on one XCD take consecutive logical tiles; the logical order
+// walks groups of kGroupM tiles along the dimension with more tiles, sweeping
+// the other dimension inside a group, so the operand with more panels is
+// streamed once while the few panels of the other stay cache-resident.
 __device__ __forceinline__ void tile_of_block(int tiles_m, int tiles_n, int &tile_m, int &tile_n) {
   const int nblk = gridDim.x, b = blockIdx.x;
   const int per = nblk / kNumXcd, rem = nblk % kNumXcd;
   const int xcd = b % kNumXcd, idx = b / kNumXcd;
   const int logical = xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
-  const int in_group = kGroupM * tiles_n;
-  const int first_m = (logical / in_group) * kGroupM;
-  const int gm = min(tiles_m - first_m, kGroupM);
+  const bool swap = tiles_n > tiles_m;
+  const int ta = swap ? tiles_n : tiles_m, tb = swap ? tiles_m : tiles_n;  // grouped, swept
+  const int in_group = kGroupM * tb;
+  const int first = (logical / in_group) * kGroupM;
+  const int g = min(ta - first, kGroupM);
   const int r = logical % in_group;
-  tile_m = first_m + r % gm;
-  tile_n = r / gm;
+  const int a = first + r % g, c = r / g;
+  tile_m = swap ? c : a;
+  tile_n = swap ? a : c;
 }
 
 // ----------------------------------------------------------------- kernel

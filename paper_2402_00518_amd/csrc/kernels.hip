@@ -501,17 +501,13 @@ hipError_t run_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Param
     return launch_gemm<T, AK, BKM, Epi, CfgSmall>(A, B, s, ep, stream);
 }
 
-int gemm_tile_rows(bool f32, bool a_kmajor, bool b_kmajor) {
-  (void)a_kmajor;
-  (void)b_kmajor;
-  return f32 ? CfgSmall::BM : CfgBig::BM;
-}
+int gemm_part_cols(bool f32) { return f32 ? CfgSmall::WN : CfgBig::WN; }
 
 hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, int n, int h, void *P, int ldn,
                        float *part_m, float *part_l, float *tgt, const int32_t *targets, hipStream_t stream) {
   EE_DISPATCH(f32, {
     typename EpiLogits<T>::Params ep{static_cast<T *>(P), ldn, part_m, part_l, tgt, targets};
-    return run_gemm<T, true, true, EpiLogits<T>>(Operand{w_out, h}, Operand{z, h}, GemmShape{vocab, n, h}, ep,
+    return run_gemm<T, true, true, EpiLogits<T>>(Operand{z, h}, Operand{w_out, h}, GemmShape{n, vocab, h}, ep,
                                                     stream);
   });
   return hipSuccess;
@@ -523,8 +519,8 @@ hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, in
   EE_DISPATCH(f32, {
     typename EpiWeightGrad<T>::Params ep{dw,   h,         static_cast<const T *>(gain), static_cast<const T *>(w),
                                          part, accumulate, gsum, static_cast<const T *>(bias), part_b};
-    return run_gemm<T, true, true, EpiWeightGrad<T>>(Operand{g_t, ldn}, Operand{xhat_t, ldn},
-                                                        GemmShape{m, h, ldn}, ep, stream);
+    return run_gemm<T, true, true, EpiWeightGrad<T>>(Operand{xhat_t, ldn}, Operand{g_t, ldn},
+                                                        GemmShape{h, m, ldn}, ep, stream);
   });
   return hipSuccess;
 }
@@ -535,7 +531,7 @@ hipError_t gemm_weight_grad_mn(bool f32, const void *g, const void *xhat, int m,
   EE_DISPATCH(f32, {
     typename EpiWeightGrad<T>::Params ep{dw, h, static_cast<const T *>(gain), static_cast<const T *>(w), part,
                                          accumulate};
-    return run_gemm<T, false, false, EpiWeightGrad<T>>(Operand{g, m}, Operand{xhat, h}, GemmShape{m, h, n},
+    return run_gemm<T, false, false, EpiWeightGrad<T>>(Operand{xhat, h}, Operand{g, m}, GemmShape{h, m, n},
                                                           ep, stream);
   });
   return hipSuccess;

@@ -10,9 +10,9 @@ namespace ee {
 
 constexpr int kTokenPad = 64;     // padding of the token dimension
 
-// Rows of the output tile of the GEMM for this dtype and operand layout (the
-// softmax and gain-gradient partials come one per tile row-block).
-int gemm_tile_rows(bool f32, bool a_kmajor, bool b_kmajor);
+// Width of the column slices over which the logits and weight-gradient
+// GEMMs keep their softmax and gain-gradient partials (one wave's columns).
+int gemm_part_cols(bool f32);
 
 // Row statistics of the exit norm.  RMSNorm (mu == NULL): r[n] =
 // (mean_j x[n][j]^2 + eps)^(-1/2).  LayerNorm: mu[n] = mean_j x[n][j] and
