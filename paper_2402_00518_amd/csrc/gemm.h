@@ -382,7 +382,7 @@ struct TileCtx {
   int m0, n0;          // tile origin
   int tile_m, tile_n;  // tile indices
   int wave_m, wave_n, lane;
-  char *smem;          // LDS free for the epilogue (>= WAVES_M * BN floats)
+  char *smem;          // the tile's LDS (two stages), free for the epilogue after a barrier
   int kz = 0;          // split-K slice of this block (epilogues that support splits offset by it)
 
   __device__ __forceinline__ int row(int i, int v) const {
@@ -392,29 +392,6 @@ struct TileCtx {
   // column index inside the tile
   __device__ __forceinline__ int tcol(int j) const { return wave_n * Cfg::WN + j * 32 + (lane & 31); }
 };
-
-// Column reduction of per-lane partial values over the tile's BM rows: lanes
-// l and l+32 hold the same column, and the wave rows meet in LDS.  `part[j]`
-// is the lane's partial for its column j; on return it holds the tile total.
-template <bool IsMax, class Cfg>
-__device__ __forceinline__ void tile_col_reduce(const TileCtx<Cfg> &t, float (&part)[Cfg::NB]) {
-  float *red = reinterpret_cast<float *>(t.smem);
-  static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE {
-    const float o = __shfl_xor(part[j], 32);
-    part[j] = IsMax ? fmaxf(part[j], o) : part[j] + o;
-  });
-  if (t.lane < 32) static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE { red[t.wave_m * Cfg::BN + t.tcol(j)] = part[j]; });
-  __syncthreads();
-  static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE {
-    float a = red[t.tcol(j)];
-    static_for<Cfg::WAVES_M - 1>([&](auto w) EE_ALWAYS_INLINE {
-      const float b = red[(w + 1) * Cfg::BN + t.tcol(j)];
-      a = IsMax ? fmaxf(a, b) : a + b;
-    });
-    part[j] = a;
-  });
-  __syncthreads();
-}
 
 // Logical tile of this block (XCD-aware, grouped order).  Blocks that run
 // together on one XCD take consecutive logical tiles; the logical order
