@@ -109,6 +109,8 @@ CASES = [
     ("embedding_f32", W.EXIT_EMBEDDING, 2, 64, 129, 0, "f32"),
     ("layernorm_bias", W.EXIT_NORM, 9, 192, 1000, 0, "bf16"),
     ("layernorm_bias_f32", W.EXIT_NORM, 4, 64, 333, 0, "f32"),
+    ("norm_max_hidden", W.EXIT_NORM, 3, 32768, 500, 0, "bf16"),
+    ("mlp_max_hidden", W.EXIT_MLP, 5, 8192, 300, 256, "bf16"),
 ]
 
 

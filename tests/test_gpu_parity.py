@@ -112,6 +112,10 @@ SMALL_CASES = [
     ("norm_multi_tile", W.EXIT_NORM, 1000, 512, 2000, 0, "bf16", False),
     # every MLP GEMM spans several 256-wide tiles with ragged M, N and K
     ("mlp_multi_tile", W.EXIT_MLP, 600, 320, 1100, 704, "bf16", False),
+    # the widest rows the ABI accepts: hidden 32768 (K of the logits GEMM,
+    # M of dW_out), and 8192 for an MLP exit (the norm backward's limit)
+    ("norm_max_hidden", W.EXIT_NORM, 40, 32768, 200, 0, "bf16", False),
+    ("mlp_max_hidden", W.EXIT_MLP, 96, 8192, 300, 256, "bf16", False),
 ]
 
 
