@@ -43,10 +43,8 @@ def kernel_flops(w, name):
         "up projection + swiglu": 2 * N * h * I,
         "down projection + residual": 2 * N * h * I,
         "dZ": 2 * N * h * V,
-        "dA + swiglu backward": 2 * N * h * I,
-        "down gradient": 2 * N * h * I,
-        "gate gradient": 2 * N * h * I,
-        "up gradient": 2 * N * h * I,
+        "dA + swiglu backward, down gradient": 2 * 2 * N * h * I,
+        "gate and up gradients": 2 * 2 * N * h * I,
     }
     return table.get(name)
 

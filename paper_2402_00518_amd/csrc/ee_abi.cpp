@@ -369,13 +369,12 @@ ee_status run_backward(const ee_exit &e, int64_t n64, void *ws, const ee_exit_gr
   EE_LAUNCH("dZ", s, ee::gemm_dz(f32, at(ws, L.P), e.w_out, n, ldn, h, V, atf(ws, L.dz), s, L.dzs));
   EE_LAUNCH("exit norm backward", s, ee::launch_norm_bwd(f32, atf(ws, L.dz), atf(ws, L.y), atf(ws, L.r), e.gamma, n, h, at(ws, L.dy), s,
                                                          L.dzs, static_cast<int64_t>(n) * h));
-  EE_LAUNCH("dA + swiglu backward", s, ee::gemm_da_swiglu(f32, at(ws, L.dy), e.w_down, n, I, h, at(ws, L.hg), at(ws, L.hu), at(ws, L.dhg),
-                            at(ws, L.dhu), s));
-  EE_LAUNCH("down gradient", s, ee::gemm_dw_down(f32, at(ws, L.dy), at(ws, L.act), n, h, I, g.d_w_down, acc, s));
-  EE_LAUNCH("gate gradient", s, ee::gemm_weight_grad_mn(f32, at(ws, L.dhg), at(ws, L.uhat), I, h, n, e.gamma_mlp, e.w_gate, g.d_w_gate,
-                                 atf(ws, L.dgpg), acc, s));
-  EE_LAUNCH("up gradient", s, ee::gemm_weight_grad_mn(f32, at(ws, L.dhu), at(ws, L.uhat), I, h, n, e.gamma_mlp, e.w_up, g.d_w_up,
-                                 atf(ws, L.dgpu), acc, s));
+  EE_LAUNCH("dA + swiglu backward, down gradient", s,
+            ee::gemm_da_swiglu_dw_down(f32, at(ws, L.dy), e.w_down, n, I, h, at(ws, L.hg), at(ws, L.hu), at(ws, L.dhg),
+                                       at(ws, L.dhu), at(ws, L.act), g.d_w_down, acc, s));
+  EE_LAUNCH("gate and up gradients", s,
+            ee::gemm_weight_grad_mn_pair(f32, at(ws, L.dhg), at(ws, L.dhu), at(ws, L.uhat), I, h, n, e.gamma_mlp, e.w_gate,
+                                         e.w_up, g.d_w_gate, g.d_w_up, atf(ws, L.dgpg), atf(ws, L.dgpu), acc, s));
   EE_LAUNCH("mlp gain gradient", s, ee::launch_gain_reduce(atf(ws, L.dgpg), static_cast<int>(L.itiles), atf(ws, L.dgpu),
                                 static_cast<int>(L.itiles), h, g.d_gamma_mlp, acc, s));
   return EE_OK;

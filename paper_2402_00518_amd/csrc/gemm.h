@@ -398,8 +398,7 @@ struct TileCtx {
 // walks groups of kGroupM tiles along the dimension with more tiles, sweeping
 // the other dimension inside a group, so the operand with more panels is
 // streamed once while the few panels of the other stay cache-resident.
-__device__ __forceinline__ void tile_of_block(int tiles_m, int tiles_n, int &tile_m, int &tile_n) {
-  const int nblk = gridDim.x, b = blockIdx.x;
+__device__ __forceinline__ void tile_of_block(int b, int nblk, int tiles_m, int tiles_n, int &tile_m, int &tile_n) {
   const int per = nblk / kNumXcd, rem = nblk % kNumXcd;
   const int xcd = b % kNumXcd, idx = b / kNumXcd;
   const int logical = xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
@@ -415,17 +414,18 @@ __device__ __forceinline__ void tile_of_block(int tiles_m, int tiles_n, int &til
 }
 
 // ----------------------------------------------------------------- kernel
+// Block b of nblk (b mod 8 = the XCD it runs on) of one GEMM problem, split-K
+// slice kz: main loop and epilogue of its tile.
 template <typename T, bool AK, bool BKM, class Epi, class Cfg>
-__global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Operand A, Operand B, GemmShape s,
-                                                                typename Epi::Params ep) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * Cfg::STAGE_BYTES];
+__device__ __forceinline__ void gemm_block(const Operand &A, const Operand &B, const GemmShape &s,
+                                           const typename Epi::Params &ep, int b, int nblk, int kz, char *smem) {
   constexpr int BK = 8 * Elem<T>::CH;
   constexpr int MB = Cfg::MB, NB = Cfg::NB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wave_m = wave / Cfg::WAVES_N, wave_n = wave % Cfg::WAVES_N;
   const int tiles_m = cdiv(s.M, Cfg::BM), tiles_n = cdiv(s.N, Cfg::BN);
   int tile_m, tile_n;
-  tile_of_block(tiles_m, tiles_n, tile_m, tile_n);
+  tile_of_block(b, nblk, tiles_m, tiles_n, tile_m, tile_n);
   const int m0 = tile_m * Cfg::BM, n0 = tile_n * Cfg::BN;
   const T *a_ptr = static_cast<const T *>(A.ptr);
   const T *b_ptr = static_cast<const T *>(B.ptr);
@@ -460,7 +460,6 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
   // for LDS.  The code of a stage has no branches (loads past the last
   // stage re-read it), so the scheduler sees each stage as one region.
   constexpr int B_OFF = Cfg::BM * kRowBytes;
-  const int kz = blockIdx.z;
   const int kbeg = s.kchunk > 0 ? kz * s.kchunk : 0;
   const int kend = s.kchunk > 0 ? min(s.K, kbeg + s.kchunk) : s.K;
   const int nk = cdiv(kend - kbeg, BK);
@@ -526,15 +525,46 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
 }
 
 template <typename T, bool AK, bool BKM, class Epi, class Cfg>
+__global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Operand A, Operand B, GemmShape s,
+                                                                typename Epi::Params ep) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * Cfg::STAGE_BYTES];
+  gemm_block<T, AK, BKM, Epi, Cfg>(A, B, s, ep, blockIdx.x, gridDim.x, blockIdx.z, smem);
+}
+
+// Two independent problems in one grid: blocks [0, blocks1) take problem 1,
+// blocks [base2, gridDim.x) problem 2, where base2 = blocks1 rounded up to a
+// multiple of 8 (the blocks in between do nothing), so that both keep the
+// XCD-aware tile order.  The hardware dispatches blocks in order, so the
+// problems share the GPU only where the first one's last round of tiles
+// leaves CUs idle.  No split K.
+template <typename T, bool AK1, bool BKM1, class Epi1, bool AK2, bool BKM2, class Epi2, class Cfg>
+__global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_pair_kernel(
+    Operand A1, Operand B1, GemmShape s1, typename Epi1::Params ep1, Operand A2, Operand B2, GemmShape s2,
+    typename Epi2::Params ep2, int blocks1, int base2) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * Cfg::STAGE_BYTES];
+  const int b = blockIdx.x;
+  if (b < blocks1)
+    gemm_block<T, AK1, BKM1, Epi1, Cfg>(A1, B1, s1, ep1, b, blocks1, 0, smem);
+  else if (b >= base2)
+    gemm_block<T, AK2, BKM2, Epi2, Cfg>(A2, B2, s2, ep2, b - base2, gridDim.x - base2, 0, smem);
+}
+
+// Shapes the loaders handle.
+template <typename T, bool AK, bool BKM>
+bool gemm_shape_ok(const Operand &A, const Operand &B, const GemmShape &s) {
+  constexpr int BK = 8 * Elem<T>::CH;
+  if (((AK || BKM) && s.K % BK != 0) || (!AK && s.M % 8 != 0) || (!BKM && s.N % 8 != 0)) return false;
+  // MN-major loaders keep signed 24-bit k-row strides
+  return !((!AK && A.ld >= (int64_t{1} << 22)) || (!BKM && B.ld >= (int64_t{1} << 22)));
+}
+
+template <typename T, bool AK, bool BKM, class Epi, class Cfg>
 hipError_t launch_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Params &ep,
                        hipStream_t stream) {
   const int64_t blocks = static_cast<int64_t>(cdiv(s.M, Cfg::BM)) * cdiv(s.N, Cfg::BN);
   if (blocks <= 0) return hipSuccess;
   constexpr int BK = 8 * Elem<T>::CH;
-  if (((AK || BKM) && s.K % BK != 0) || (!AK && s.M % 8 != 0) || (!BKM && s.N % 8 != 0))
-    return hipErrorInvalidValue;  // shapes the loaders do not handle
-  if ((!AK && A.ld >= (int64_t{1} << 22)) || (!BKM && B.ld >= (int64_t{1} << 22)))
-    return hipErrorInvalidValue;  // MN-major loaders keep signed 24-bit k-row strides
+  if (!gemm_shape_ok<T, AK, BKM>(A, B, s)) return hipErrorInvalidValue;
   int splits = 1;
   if (s.kchunk > 0) {
     if (s.kchunk % BK != 0) return hipErrorInvalidValue;  // slices start on stage boundaries
@@ -542,6 +572,23 @@ hipError_t launch_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Pa
   }
   hipLaunchKernelGGL((gemm_kernel<T, AK, BKM, Epi, Cfg>), dim3(static_cast<unsigned>(blocks), 1, splits),
                      dim3(Cfg::THREADS), 0, stream, A, B, s, ep);
+  return hipGetLastError();
+}
+
+template <typename T, bool AK1, bool BKM1, class Epi1, bool AK2, bool BKM2, class Epi2, class Cfg>
+hipError_t launch_gemm_pair(Operand A1, Operand B1, GemmShape s1, const typename Epi1::Params &ep1, Operand A2,
+                            Operand B2, GemmShape s2, const typename Epi2::Params &ep2, hipStream_t stream) {
+  const int64_t b1 = static_cast<int64_t>(cdiv(s1.M, Cfg::BM)) * cdiv(s1.N, Cfg::BN);
+  const int64_t b2 = static_cast<int64_t>(cdiv(s2.M, Cfg::BM)) * cdiv(s2.N, Cfg::BN);
+  if (s1.kchunk != 0 || s2.kchunk != 0) return hipErrorInvalidValue;
+  if (b1 <= 0) return launch_gemm<T, AK2, BKM2, Epi2, Cfg>(A2, B2, s2, ep2, stream);
+  if (b2 <= 0) return launch_gemm<T, AK1, BKM1, Epi1, Cfg>(A1, B1, s1, ep1, stream);
+  if (!gemm_shape_ok<T, AK1, BKM1>(A1, B1, s1) || !gemm_shape_ok<T, AK2, BKM2>(A2, B2, s2))
+    return hipErrorInvalidValue;
+  const int64_t base2 = (b1 + kNumXcd - 1) / kNumXcd * kNumXcd;
+  hipLaunchKernelGGL((gemm_pair_kernel<T, AK1, BKM1, Epi1, AK2, BKM2, Epi2, Cfg>),
+                     dim3(static_cast<unsigned>(base2 + b2)), dim3(Cfg::THREADS), 0, stream, A1, B1, s1, ep1, A2,
+                     B2, s2, ep2, static_cast<int>(b1), static_cast<int>(base2));
   return hipGetLastError();
 }
 

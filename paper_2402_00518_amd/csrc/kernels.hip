@@ -501,6 +501,15 @@ hipError_t run_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Param
     return launch_gemm<T, AK, BKM, Epi, CfgSmall>(A, B, s, ep, stream);
 }
 
+template <typename T, bool AK1, bool BKM1, class Epi1, bool AK2, bool BKM2, class Epi2>
+hipError_t run_gemm_pair(Operand A1, Operand B1, GemmShape s1, const typename Epi1::Params &ep1, Operand A2,
+                         Operand B2, GemmShape s2, const typename Epi2::Params &ep2, hipStream_t stream) {
+  if constexpr (std::is_same<T, bf16_t>::value)
+    return launch_gemm_pair<T, AK1, BKM1, Epi1, AK2, BKM2, Epi2, CfgBig>(A1, B1, s1, ep1, A2, B2, s2, ep2, stream);
+  else
+    return launch_gemm_pair<T, AK1, BKM1, Epi1, AK2, BKM2, Epi2, CfgSmall>(A1, B1, s1, ep1, A2, B2, s2, ep2, stream);
+}
+
 int gemm_part_cols(bool f32) { return f32 ? CfgSmall::WN : CfgBig::WN; }
 
 hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, int n, int h, void *P, int ldn,
@@ -525,14 +534,16 @@ hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, in
   return hipSuccess;
 }
 
-hipError_t gemm_weight_grad_mn(bool f32, const void *g, const void *xhat, int m, int h, int n,
-                               const void *gain, const void *w, float *dw, float *part, int accumulate,
-                               hipStream_t stream) {
+hipError_t gemm_weight_grad_mn_pair(bool f32, const void *g1, const void *g2, const void *xhat, int m, int h, int n,
+                                   const void *gain, const void *w1, const void *w2, float *dw1, float *dw2,
+                                   float *part1, float *part2, int accumulate, hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiWeightGrad<T>::Params ep{dw, h, static_cast<const T *>(gain), static_cast<const T *>(w), part,
-                                         accumulate};
-    return run_gemm<T, false, false, EpiWeightGrad<T>>(Operand{xhat, h}, Operand{g, m}, GemmShape{h, m, n},
-                                                          ep, stream);
+    const T *gn = static_cast<const T *>(gain);
+    typename EpiWeightGrad<T>::Params e1{dw1, h, gn, static_cast<const T *>(w1), part1, accumulate};
+    typename EpiWeightGrad<T>::Params e2{dw2, h, gn, static_cast<const T *>(w2), part2, accumulate};
+    return run_gemm_pair<T, false, false, EpiWeightGrad<T>, false, false, EpiWeightGrad<T>>(
+        Operand{xhat, h}, Operand{g1, m}, GemmShape{h, m, n}, e1, Operand{xhat, h}, Operand{g2, m},
+        GemmShape{h, m, n}, e2, stream);
   });
   return hipSuccess;
 }
@@ -592,23 +603,16 @@ hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn,
   return hipSuccess;
 }
 
-hipError_t gemm_da_swiglu(bool f32, const void *dy, const void *w_down, int n, int inter, int h, const void *hg,
-                          const void *hu, void *dhg, void *dhu, hipStream_t stream) {
+hipError_t gemm_da_swiglu_dw_down(bool f32, const void *dy, const void *w_down, int n, int inter, int h,
+                                 const void *hg, const void *hu, void *dhg, void *dhu, const void *act, float *dwd,
+                                 int accumulate, hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiSwiGLUBwdTr<T>::Params ep{static_cast<const T *>(hg), static_cast<const T *>(hu),
+    typename EpiSwiGLUBwdTr<T>::Params e1{static_cast<const T *>(hg), static_cast<const T *>(hu),
                                           static_cast<T *>(dhg), static_cast<T *>(dhu), inter};
-    return run_gemm<T, false, true, EpiSwiGLUBwdTr<T>>(Operand{w_down, inter}, Operand{dy, h},
-                                                          GemmShape{inter, n, h}, ep, stream);
-  });
-  return hipSuccess;
-}
-
-hipError_t gemm_dw_down(bool f32, const void *dy, const void *act, int n, int h, int inter, float *dwd,
-                        int accumulate, hipStream_t stream) {
-  EE_DISPATCH(f32, {
-    typename EpiStoreF32<T>::Params ep{dwd, inter, h, accumulate};
-    return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{dy, h}, Operand{act, inter},
-                                                        GemmShape{h, inter, n}, ep, stream);
+    typename EpiStoreF32<T>::Params e2{dwd, inter, h, accumulate};
+    return run_gemm_pair<T, false, true, EpiSwiGLUBwdTr<T>, false, false, EpiStoreF32<T>>(
+        Operand{w_down, inter}, Operand{dy, h}, GemmShape{inter, n, h}, e1, Operand{dy, h}, Operand{act, inter},
+        GemmShape{h, inter, n}, e2, stream);
   });
   return hipSuccess;
 }

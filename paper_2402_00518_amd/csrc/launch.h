@@ -85,10 +85,13 @@ hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, in
                                const void *gain, const void *w, float *dw, float *part, int accumulate,
                                hipStream_t stream, const float *gsum = nullptr, const void *bias = nullptr,
                                float *part_b = nullptr);
-// Same, operands stored row-major over tokens: g [n][m], xhat [n][h].
-hipError_t gemm_weight_grad_mn(bool f32, const void *g, const void *xhat, int m, int h, int n,
-                               const void *gain, const void *w, float *dw, float *part, int accumulate,
-                               hipStream_t stream);
+// Two such weight gradients that share x_hat and the gain, operands stored
+// row-major over tokens (g1, g2 [n][m], xhat [n][h]): the gate and up
+// gradients of the MLP exit, one launch (the second problem's tiles follow
+// the first's, filling the CUs its last round leaves idle).
+hipError_t gemm_weight_grad_mn_pair(bool f32, const void *g1, const void *g2, const void *xhat, int m, int h, int n,
+                                   const void *gain, const void *w1, const void *w2, float *dw1, float *dw2,
+                                   float *part1, float *part2, int accumulate, hipStream_t stream);
 // H_g[n][I] = U W_gate^T.
 hipError_t gemm_gate(bool f32, const void *u, const void *w_gate, int n, int inter, int h, void *hg,
                      hipStream_t stream);
@@ -105,12 +108,12 @@ int dz_splits(bool f32, int ldn, int h, int vocab);
 int dz_kchunk(int vocab, int splits);
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab,
                    float *dz, hipStream_t stream, int splits = 1);
-// dA = dY W_down with the SwiGLU backward epilogue.
-hipError_t gemm_da_swiglu(bool f32, const void *dy, const void *w_down, int n, int inter, int h,
-                          const void *hg, const void *hu, void *dhg, void *dhu, hipStream_t stream);
-// dW_down[h][I] (=|+=) dY^T A.
-hipError_t gemm_dw_down(bool f32, const void *dy, const void *act, int n, int h, int inter, float *dwd,
-                        int accumulate, hipStream_t stream);
+// One launch of two independent products of the MLP backward:
+//   dA = dY W_down with the SwiGLU backward epilogue (dH_g, dH_u), and
+//   dW_down[h][I] (=|+=) dY^T A.
+hipError_t gemm_da_swiglu_dw_down(bool f32, const void *dy, const void *w_down, int n, int inter, int h,
+                                 const void *hg, const void *hu, void *dhg, void *dhu, const void *act, float *dwd,
+                                 int accumulate, hipStream_t stream);
 
 // ------------------------------------------------------------- optimizer
 // One tensor of a fused Adam launch (optim.hip).  Pointers are device

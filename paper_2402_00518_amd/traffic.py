@@ -28,23 +28,19 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
-# Profiling label -> (substring of the demangled kernel name, slot).  Kernels
-# that share one instantiation within an exit's step alternate in launch
-# order (dZ before the down-projection gradient, gate before up gradient):
-# slot = index of the launch modulo 2 among that instantiation's launches.
+# Profiling label -> substring of the demangled kernel name (one launch per
+# exit and step each).
 LABEL_KERNELS = {
-    "logits + softmax partials": ("ee::EpiLogits<", None),
-    "output-matrix gradient": ("true, true, ee::EpiWeightGrad<", None),
-    "dZ": ("false, false, ee::EpiStoreF32<", 0),
-    "down gradient": ("false, false, ee::EpiStoreF32<", 1),
-    "gate gradient": ("false, false, ee::EpiWeightGrad<", 0),
-    "up gradient": ("false, false, ee::EpiWeightGrad<", 1),
-    "gate projection": ("ee::EpiStoreTr<", None),
-    "up projection + swiglu": ("ee::EpiSwiGLU<", None),
-    "down projection + residual": ("ee::EpiResidualTr<", None),
-    "dA + swiglu backward": ("ee::EpiSwiGLUBwdTr<", None),
-    "logit seed": ("seed_kernel", None),
-    "cross-entropy reduce": ("ce_reduce_kernel", None),
+    "logits + softmax partials": "ee::EpiLogits<",
+    "output-matrix gradient": "gemm_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
+    "dZ": "gemm_kernel<unsigned short, false, false, ee::EpiStoreF32<",
+    "gate and up gradients": "gemm_pair_kernel<unsigned short, false, false, ee::EpiWeightGrad<",
+    "gate projection": "ee::EpiStoreTr<",
+    "up projection + swiglu": "ee::EpiSwiGLU<",
+    "down projection + residual": "ee::EpiResidualTr<",
+    "dA + swiglu backward, down gradient": "ee::EpiSwiGLUBwdTr<",
+    "logit seed": "seed_kernel",
+    "cross-entropy reduce": "ce_reduce_kernel",
 }
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
@@ -82,20 +78,11 @@ def copy_factor(rows, copy_bytes: int, copies: int) -> tuple[float, float]:
 
 def per_label(rows):
     """Mean counter KiB per dispatch for every label of LABEL_KERNELS."""
-    seen = defaultdict(int)
     acc = defaultdict(list)
     for _, name, v in rows:
-        for label, (pat, slot) in LABEL_KERNELS.items():
-            if pat not in name:
-                continue
-            if slot is None:
-                acc[label].append(v)
-            else:
-                if seen[pat] % 2 == slot:
-                    acc[label].append(v)
-        for pat in {p for p, s in LABEL_KERNELS.values() if s is not None}:
+        for label, pat in LABEL_KERNELS.items():
             if pat in name:
-                seen[pat] += 1
+                acc[label].append(v)
     return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
 
 
