@@ -44,30 +44,21 @@ constexpr int kRowBytes = 128;
 constexpr int kNumXcd = 8;
 constexpr int kGroupM = 4;
 
-template <int BM_, int BN_, int WM_, int WN_, int MIN_BLOCKS_, int PGR_>
+template <int BM_, int BN_, int WM_, int WN_, int MIN_BLOCKS_>
 struct TileCfg {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr int MIN_BLOCKS = MIN_BLOCKS_;  // workgroups per CU the registers must allow
-  static constexpr int PGR = PGR_;                // stages of global loads in flight (register sets)
   static constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN;
   static constexpr int THREADS = WAVES_M * WAVES_N * 64;
   static constexpr int MB = WM / 32, NB = WN / 32;
   static constexpr int STAGE_BYTES = (BM + BN) * kRowBytes;
 };
 // 128 x 128 tile, 64 x 64 per wave: any operand layout, bf16 or fp32.
-using CfgSmall = TileCfg<128, 128, 64, 64, 2, 1>;
-// 256 x 256 tile, 8 waves of 128 x 64 (two waves per SIMD): K-major bf16
-// operands.  1.5x the MFMA work per byte read from LDS of the small tile,
-// and a second wave per SIMD to issue while the other waits.
-using CfgBig8 = TileCfg<256, 256, 128, 64, 1, 1>;
-// 256 x 256 tile, 4 waves of 128 x 128 with two stages of global loads in
-// flight: twice the MFMA work per LDS byte of the small tile, and enough
-// loads outstanding to cover the latency of L2 misses.
-using CfgBig4 = TileCfg<256, 256, 128, 128, 1, 1>;
-#ifndef EE_BIG_CFG
-#define EE_BIG_CFG CfgBig8
-#endif
-using CfgBig = EE_BIG_CFG;
+using CfgSmall = TileCfg<128, 128, 64, 64, 2>;
+// 256 x 256 tile, 8 waves of 128 x 64 (two waves per SIMD): every bf16 GEMM.
+// 1.5x the MFMA work per byte read from LDS of the small tile, and a second
+// wave per SIMD to issue while the other waits.
+using CfgBig = TileCfg<256, 256, 128, 64, 1>;
 
 template <typename T> struct Elem;
 template <> struct Elem<bf16_t> {

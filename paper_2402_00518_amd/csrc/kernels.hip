@@ -227,55 +227,86 @@ __device__ __forceinline__ void lse_merge(float &m, float &l, float m2, float l2
   m = mn;
 }
 
-__global__ __launch_bounds__(256) void ce_reduce_kernel(CeReduceArgs a) {
-  __shared__ float sm_m[8][32], sm_l[8][32];
-  const int tk = threadIdx.x & 31, tg = threadIdx.x >> 5;
-  const int n = blockIdx.x * 32 + tk;
-  float m = -INFINITY, l = 0.0f;
-  if (n < a.n) {
-    // Tiles t = tg, tg + 8, ...: four rows' loads are issued before they are
-    // merged (in tile order), so the loop is not one load latency per tile.
-    int t = tg;
-    for (; t + 24 < a.tiles; t += 32) {
-      float pm[4], pl[4];
+// 32 tokens per block: 8 threads of 4 consecutive tokens (16-byte loads) x 64
+// groups of slices (slices g, g + 64, ... of group g, all loads in flight),
+// merged through LDS in group order, so the result does not depend on timing.
+constexpr int kCeGroups = 64;
+constexpr int kCeSlicesPerThread = 8;  // up to kCeGroups * 8 slices in one round of loads
+
+__global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
+  __shared__ float sm_m[kCeGroups][32], sm_l[kCeGroups][32];
+  const int tt = threadIdx.x & 7, g = threadIdx.x >> 3;
+  const int n0 = blockIdx.x * 32 + tt * 4;  // < ldn: partials are padded to ldn tokens
+  // Each thread: max over its slices, then the sum of l exp(m - max) (one
+  // exponential per slice, no chain of merges).
+  float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, l[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int t0 = g; t0 < a.tiles; t0 += kCeGroups * kCeSlicesPerThread) {
+    f32x4_t pm[kCeSlicesPerThread], pl[kCeSlicesPerThread];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t o = static_cast<int64_t>(t + 8 * q) * a.ldn + n;
-        pm[q] = a.part_m[o];
-        pl[q] = a.part_l[o];
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) lse_merge(m, l, pm[q], pl[q]);
+    for (int q = 0; q < kCeSlicesPerThread; ++q) {
+      const int t = t0 + q * kCeGroups;
+      const int64_t o = static_cast<int64_t>(min(t, a.tiles - 1)) * a.ldn + n0;
+      pm[q] = *reinterpret_cast<const f32x4_t *>(a.part_m + o);
+      pl[q] = *reinterpret_cast<const f32x4_t *>(a.part_l + o);
     }
-    for (; t < a.tiles; t += 8) {
-      const int64_t o = static_cast<int64_t>(t) * a.ldn + n;
-      lse_merge(m, l, a.part_m[o], a.part_l[o]);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < kCeSlicesPerThread; ++q)
+        if (t0 + q * kCeGroups < a.tiles) mx = fmaxf(mx, pm[q][e]);
+      float sl = 0.0f;
+#pragma unroll
+      for (int q = 0; q < kCeSlicesPerThread; ++q)
+        if (t0 + q * kCeGroups < a.tiles && pl[q][e] > 0.0f) sl += pl[q][e] * fast_exp(pm[q][e] - mx);
+      lse_merge(m[e], l[e], mx, sl);
     }
   }
-  sm_m[tg][tk] = m;
-  sm_l[tg][tk] = l;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    sm_m[g][tt * 4 + e] = m[e];
+    sm_l[g][tt * 4 + e] = l[e];
+  }
   __syncthreads();
-  if (tg != 0) return;
-  float contrib = 0.0f;
-  if (n < a.n) {
-    m = sm_m[0][tk];
-    l = sm_l[0][tk];
-    for (int g = 1; g < 8; ++g) lse_merge(m, l, sm_m[g][tk], sm_l[g][tk]);
-    const float lse = m + logf(l);
-    const int y = a.targets[n];
-    const bool ok = y >= 0 && y < a.vocab;
-    if (!ok) *a.flag = 1;
-    const float nll = ok ? lse - a.tgt[n] : NAN;
-    float w = a.token_w != nullptr ? a.token_w[n] : 1.0f;
-    if (a.dynamic_weights) w *= expf(m - lse);  // detached confidence = max probability
-    a.lse[n] = lse;
-    a.sn[n] = a.exit_weight * w / static_cast<float>(a.n);
-    if (a.row_loss != nullptr) a.row_loss[n] = nll;
-    contrib = w * nll;
+  // 16 threads per token combine the 64 groups (4 each, then a fixed
+  // butterfly over the 16).
+  const int tk = threadIdx.x >> 4, sub = threadIdx.x & 15, n = blockIdx.x * 32 + tk;
+  float mm = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) mm = fmaxf(mm, sm_m[sub * 4 + q][tk]);
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) mm = fmaxf(mm, __shfl_xor(mm, o, 16));
+  float ll = 0.0f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float lq = sm_l[sub * 4 + q][tk];
+    if (lq > 0.0f) ll += lq * fast_exp(sm_m[sub * 4 + q][tk] - mm);
   }
 #pragma unroll
-  for (int o = 16; o > 0; o >>= 1) contrib += __shfl_xor(contrib, o, 32);
-  if (tk == 0) a.block_sums[blockIdx.x] = contrib;
+  for (int o = 8; o > 0; o >>= 1) ll += __shfl_xor(ll, o, 16);
+  if (sub == 0) {
+    float contrib = 0.0f;
+    if (n < a.n) {
+      const float lse = mm + logf(ll);
+      const int y = a.targets[n];
+      const bool ok = y >= 0 && y < a.vocab;
+      if (!ok) *a.flag = 1;
+      const float nll = ok ? lse - a.tgt[n] : NAN;
+      float w = a.token_w != nullptr ? a.token_w[n] : 1.0f;
+      if (a.dynamic_weights) w *= expf(mm - lse);  // detached confidence = max probability
+      a.lse[n] = lse;
+      a.sn[n] = a.exit_weight * w / static_cast<float>(a.n);
+      if (a.row_loss != nullptr) a.row_loss[n] = nll;
+      contrib = w * nll;
+    }
+    sm_m[0][tk] = contrib;  // group 0's maxima were consumed above
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float total = 0.0f;
+    for (int q = 0; q < 32; ++q) total += sm_m[0][q];
+    a.block_sums[blockIdx.x] = total;
+  }
 }
 
 // In-place seed: each thread owns 8 consecutive tokens of 16 vocab rows (one
@@ -360,34 +391,55 @@ __global__ __launch_bounds__(256) void final_loss_kernel(const float *bs, int nb
 }
 
 // 32 columns x 8 groups of tiles per block; groups merge in a fixed order.
+// 32 columns per block: 8 threads of 4 consecutive columns x 32 groups of
+// rows (rows g, g + 32, ... of group g, loads in flight in batches of 8),
+// merged through LDS in group order.  Row strides that are multiples of 4
+// (the gain gradients: h is a multiple of 64) take 16-byte loads; others
+// (the vocabulary-wide row sums) take bounds-checked scalar loads.
+constexpr int kGainGroups = 32;
+
+template <bool VEC>
+__device__ __forceinline__ f32x4_t sum_rows4(const float *p, int tiles, int h, int g, int j0) {
+  f32x4_t s = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (j0 >= h) return s;
+  for (int t0 = g; t0 < tiles; t0 += kGainGroups * 8) {
+    f32x4_t v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const float *row = p + static_cast<int64_t>(min(t0 + q * kGainGroups, tiles - 1)) * h;
+      if constexpr (VEC) {
+        v[q] = *reinterpret_cast<const f32x4_t *>(row + j0);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[q][e] = j0 + e < h ? row[j0 + e] : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      if (t0 + q * kGainGroups < tiles) s += v[q];
+  }
+  return s;
+}
+
 __global__ __launch_bounds__(256) void gain_reduce_kernel(const float *pa, int ta, const float *pb, int tb,
                                                           int h, float *out, int accumulate) {
-  __shared__ float red[8][32];
-  const int c = threadIdx.x & 31, g = threadIdx.x >> 5;
-  const int j = blockIdx.x * 32 + c;
-  float s = 0.0f;
-  if (j < h) {
-    // Rows t = g, g + 8, ...: loads of four rows issued before their adds
-    // (in row order), so the loop is not one load latency per row.
-    auto sum_rows = [&](const float *p, int tiles) {
-      int t = g;
-      for (; t + 24 < tiles; t += 32) {
-        float v[4];
+  __shared__ float red[kGainGroups][32];
+  const int tc = threadIdx.x & 7, g = threadIdx.x >> 3;
+  const int j0 = blockIdx.x * 32 + tc * 4;
+  f32x4_t s;
+  with_flag(h % 4 == 0, [&](auto V_) EE_ALWAYS_INLINE {
+    constexpr bool kVec = decltype(V_)::value;
+    s = sum_rows4<kVec>(pa, ta, h, g, j0);
+    if (pb != nullptr) s += sum_rows4<kVec>(pb, tb, h, g, j0);
+  });
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = p[static_cast<int64_t>(t + 8 * q) * h + j];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) s += v[q];
-      }
-      for (; t < tiles; t += 8) s += p[static_cast<int64_t>(t) * h + j];
-    };
-    sum_rows(pa, ta);
-    sum_rows(pb, tb);
-  }
-  red[g][c] = s;
+  for (int e = 0; e < 4; ++e) red[g][tc * 4 + e] = s[e];
   __syncthreads();
-  if (g != 0 || j >= h) return;
+  if (threadIdx.x >= 32) return;
+  const int c = threadIdx.x, j = blockIdx.x * 32 + c;
+  if (j >= h) return;
   float total = red[0][c];
-  for (int k = 1; k < 8; ++k) total += red[k][c];
+  for (int q = 1; q < kGainGroups; ++q) total += red[q][c];
   out[j] = accumulate ? out[j] + total : total;
 }
 
@@ -437,7 +489,7 @@ hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, c
 }
 
 hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream) {
-  hipLaunchKernelGGL(ce_reduce_kernel, dim3(cdiv(a.n, 32)), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(ce_reduce_kernel, dim3(cdiv(a.n, 32)), dim3(512), 0, stream, a);
   return hipGetLastError();
 }
 
