@@ -29,7 +29,14 @@ namespace {
 
 constexpr int kDecRows = 32;    // rows of W per block
 constexpr int kDecTokens = 32;  // token rows per pass (grid.y walks more)
-constexpr int kDecWaves = 4;    // waves per block, each a quarter of K
+// Waves per block (each a share of K): 4 when the rows give at least two
+// blocks per CU of a 256-CU GPU, else 8 or 16, so that narrow products (the
+// MLP's down projection: 5120 rows, K = 13824) still keep enough loads in
+// flight.  A shape-only rule, so results do not depend on the device.
+constexpr int kDecWavesMax = 16;
+__host__ __device__ constexpr int dec_waves(int row_blocks) {
+  return row_blocks >= 512 ? 4 : (row_blocks >= 256 ? 8 : 16);
+}
 constexpr int kDecGroup = 8;    // fragment loads per operand per lane in flight
 
 template <typename T> struct DecFrag;
@@ -58,7 +65,7 @@ __device__ __forceinline__ int dec_row(int r0, int lane, int v) {
   return r0 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
 }
 
-template <typename T, class Epi>
+template <typename T, class Epi, int kDecWaves>
 __global__ __launch_bounds__(64 * kDecWaves) void skinny_kernel(const T *__restrict__ W, int64_t ldw, int R,
                                                                 const T *__restrict__ Z, int64_t ldz, int B, int K,
                                                                 typename Epi::Params ep) {
@@ -305,10 +312,21 @@ hipError_t launch_skinny(const void *W, int64_t ldw, int R, const void *Z, int64
                          const typename Epi::Params &ep, hipStream_t stream) {
   if (R <= 0 || B <= 0) return hipSuccess;
   if (K % (4 * DecFrag<T>::K_PER_LOAD) != 0) return hipErrorInvalidValue;
-  const dim3 grid(static_cast<unsigned>((R + kDecRows - 1) / kDecRows),
-                  static_cast<unsigned>((B + kDecTokens - 1) / kDecTokens));
-  hipLaunchKernelGGL((skinny_kernel<T, Epi>), grid, dim3(64 * kDecWaves), 0, stream, static_cast<const T *>(W), ldw,
-                     R, static_cast<const T *>(Z), ldz, B, K, ep);
+  const int row_blocks = (R + kDecRows - 1) / kDecRows;
+  const dim3 grid(static_cast<unsigned>(row_blocks), static_cast<unsigned>((B + kDecTokens - 1) / kDecTokens));
+  const T *w = static_cast<const T *>(W);
+  const T *z = static_cast<const T *>(Z);
+  switch (dec_waves(row_blocks)) {
+    case 4:
+      hipLaunchKernelGGL((skinny_kernel<T, Epi, 4>), grid, dim3(64 * 4), 0, stream, w, ldw, R, z, ldz, B, K, ep);
+      break;
+    case 8:
+      hipLaunchKernelGGL((skinny_kernel<T, Epi, 8>), grid, dim3(64 * 8), 0, stream, w, ldw, R, z, ldz, B, K, ep);
+      break;
+    default:
+      hipLaunchKernelGGL((skinny_kernel<T, Epi, kDecWavesMax>), grid, dim3(64 * kDecWavesMax), 0, stream, w, ldw, R,
+                         z, ldz, B, K, ep);
+  }
   return hipGetLastError();
 }
 
