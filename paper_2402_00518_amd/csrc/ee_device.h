@@ -67,12 +67,19 @@ template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return
 
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
 
-__device__ __forceinline__ float silu_f(float t) { return t / (1.0f + __expf(-t)); }
+// sigma(t) = 1 / (1 + exp(-t)) with the hardware exponential and reciprocal
+// (about 1 ulp each): exp(-t) overflows to +inf for t < -88, and rcp(inf) = 0
+// is the correct limit.
+__device__ __forceinline__ float sigmoid_f(float t) { return __builtin_amdgcn_rcpf(1.0f + __expf(-t)); }
 
-// d silu / dt = sigma(t) (1 + t (1 - sigma(t)))
-__device__ __forceinline__ float silu_grad_f(float t) {
-  float s = 1.0f / (1.0f + __expf(-t));
-  return s * (1.0f + t * (1.0f - s));
+__device__ __forceinline__ float silu_f(float t) { return t * sigmoid_f(t); }
+
+// silu(t) = t sigma(t) and d silu / dt = sigma(t) (1 + t (1 - sigma(t))),
+// sharing one sigmoid.
+__device__ __forceinline__ void silu_and_grad(float t, float &silu, float &grad) {
+  const float s = sigmoid_f(t);
+  silu = t * s;
+  grad = s * (1.0f + t * (1.0f - s));
 }
 
 __device__ __forceinline__ float warp_sum(float v) {

@@ -47,25 +47,40 @@ __device__ __forceinline__ void for_each_acc_loaded(f32x16_t (&acc)[Cfg::MB][Cfg
 // Row-vector form, for outputs stored transposed (C[m][n] at ptr[n*ld + m]):
 // a lane's accumulator rows 4q..4q+3 of a block are consecutive, so they
 // are one 8-byte (bf16) or 16-byte (fp32) access there.  f(row0, col, j,
-// vals, loaded) runs for every such group after all load(row0_c, col_c) of
-// the 32-row block have been issued (row0 and col clamped into the problem;
-// the row count must be a multiple of 4).
+// vals, loaded) runs for every such group of 32-row block i once the
+// load(row0_c, col_c) of the whole block are in, and the loads of block i + 1
+// are issued before block i is processed (row0 and col clamped into the
+// problem; the row count must be a multiple of 4).  A 128-byte bf16 line of
+// the output spans two blocks; with the next block's loads already in flight
+// its two halves reach L2 sooner after each other (under the main loop's
+// operand streaming a half-written line can be evicted within microseconds
+// and is then written twice).
 template <class Cfg, class L, class F>
 __device__ __forceinline__ void for_each_acc4_loaded(f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t,
                                                      L &&load, F &&f) {
   using V = decltype(load(0, 0));
+  V pre[2][4][Cfg::NB];
+  auto issue = [&](auto blk) EE_ALWAYS_INLINE {
+    constexpr int I = decltype(blk)::value;
+    if constexpr (I < Cfg::MB) {
+      static_for<4>([&](auto q) EE_ALWAYS_INLINE {
+        const int row0 = min(t.row(I, 4 * q), t.M - 4);
+        static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE {
+          pre[I % 2][decltype(q)::value][j] = load(row0, min(t.col(j), t.N - 1));
+        });
+      });
+    }
+  };
+  issue(std::integral_constant<int, 0>{});
   static_for<Cfg::MB>([&](auto i) EE_ALWAYS_INLINE {
-    V pre[4][Cfg::NB];
-    static_for<4>([&](auto q) EE_ALWAYS_INLINE {
-      const int row0 = min(t.row(i, 4 * q), t.M - 4);
-      static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE { pre[q][j] = load(row0, min(t.col(j), t.N - 1)); });
-    });
+    constexpr int I = decltype(i)::value;
+    issue(std::integral_constant<int, I + 1>{});
     static_for<4>([&](auto q) EE_ALWAYS_INLINE {
       constexpr int v0 = 4 * decltype(q)::value;
-      const int row0 = t.row(i, v0);
+      const int row0 = t.row(I, v0);
       static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE {
-        const f32x4_t c = {acc[i][j][v0], acc[i][j][v0 + 1], acc[i][j][v0 + 2], acc[i][j][v0 + 3]};
-        f(row0, t.col(j), static_cast<int>(j), c, pre[q][j]);
+        const f32x4_t c = {acc[I][j][v0], acc[I][j][v0 + 1], acc[I][j][v0 + 2], acc[I][j][v0 + 3]};
+        f(row0, t.col(j), static_cast<int>(j), c, pre[I % 2][decltype(q)::value][j]);
       });
     });
   });
@@ -87,14 +102,6 @@ __device__ __forceinline__ void store4(bf16_t *p, f32x4_t v) {
   const b16x2_t hi = __builtin_convertvector((f32x2_t{v[2], v[3]}), b16x2_t);
   *reinterpret_cast<u32x2_t *>(p) = u32x2_t{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
 }
-
-struct F2 {
-  float a, b;
-};
-
-struct V2 {
-  f32x4_t a, b;
-};
 
 // ------------------------------------------------ row-slot reductions
 // A lane holds accumulator element v of block (i, j) for NB columns j at one
@@ -138,7 +145,10 @@ __device__ __forceinline__ f32x4_t cvt4(u32x2_t u) {
                  __uint_as_float(u[1] & 0xFFFF0000u)};
 }
 __device__ __forceinline__ f32x4_t cvt4(f32x4_t v) { return v; }
-template <typename T> using Raw4 = decltype(raw4(static_cast<const T *>(nullptr)));
+template <typename T> struct Raw4Of;
+template <> struct Raw4Of<bf16_t> { using type = u32x2_t; };
+template <> struct Raw4Of<float> { using type = f32x4_t; };
+template <typename T> using Raw4 = typename Raw4Of<T>::type;
 
 // Logits: C[n][v] = S[n][v] = Z[n] . W_out[v] (rows = tokens, columns =
 // vocab ids).  For every token and every WN-column slice of the vocabulary
@@ -278,8 +288,8 @@ struct EpiLogits {
 //   dW[r][j]       += gsum[r] * b[j]               (gsum[r] = sum_n G[n][r])
 //   part_b[s][j]    = sum_{r in slice s} W[r][j] * gsum[r]   (sums to d b)
 // Rows are handled in parts of two blocks (32 slots, one row per lane after
-// the reduce-scatter); the W loads of every part are issued before the first
-// is used, so their latency is paid about once.
+// the reduce-scatter); the W loads of each 32-row block are issued while the
+// previous block is processed.
 template <typename T>
 struct EpiWeightGrad {
   struct Params {
@@ -301,6 +311,18 @@ struct EpiWeightGrad {
     const int64_t ct = cbase / Cfg::WN;
     const int rbase = t.m0 + t.wave_m * Cfg::WM + hw * 4;  // feature of the lane's slot 0
     const bool interior = t.m0 + Cfg::BM <= t.M && cbase + Cfg::WN <= t.N;
+    // The tile's gain and bias as fp32 in LDS, so that the stores below do
+    // not wait on a global load per group of four features (a line's four
+    // pieces then reach L2 close together, rather than spread over several
+    // load latencies during which it may be evicted half-written).
+    float *gl = reinterpret_cast<float *>(t.smem);  // [BM] gain, [BM] bias
+    __syncthreads();  // every wave is past its last fragment reads
+    if (threadIdx.x < Cfg::BM) {
+      const int r = min(t.m0 + static_cast<int>(threadIdx.x), t.M - 1);
+      gl[threadIdx.x] = p.gain != nullptr ? to_f32(p.gain[r]) : 1.0f;
+      gl[Cfg::BM + threadIdx.x] = p.bias != nullptr ? to_f32(p.bias[r]) : 0.0f;
+    }
+    __syncthreads();
     auto body = [&](auto IN_, auto W_, auto A_, auto B_, auto G_) EE_ALWAYS_INLINE {
       constexpr bool kIn = decltype(IN_)::value, kW = decltype(W_)::value, kAcc = decltype(A_)::value;
       constexpr bool kB = decltype(B_)::value, kG = decltype(G_)::value;
@@ -323,31 +345,33 @@ struct EpiWeightGrad {
         const int o = I * 32 + Q * 8;
         return kIn ? o : min(o, t.M - 4 - rbase);
       };
-      Raw4<T> w[NPART][2][4][NB];
-      if constexpr (kW) {
-        static_for<NPART>([&](auto hf) EE_ALWAYS_INLINE {
-          static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
-            static_for<4>([&](auto q) EE_ALWAYS_INLINE {
-              const int o = goff(decltype(hf)::value * 2 + decltype(ii)::value, decltype(q)::value);
-              static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
-                w[decltype(hf)::value][decltype(ii)::value][decltype(q)::value][j] = raw4(wcol[j] + o);
-              });
-            });
+      // W of one 32-row block, double-buffered: the block after the current
+      // one is always in flight (two blocks of registers, no spills).
+      Raw4<T> w[2][4][NB];
+      auto load_w = [&](auto blk) EE_ALWAYS_INLINE {
+        constexpr int I = decltype(blk)::value;
+        if constexpr (kW && I < Cfg::MB) {
+          static_for<4>([&](auto q) EE_ALWAYS_INLINE {
+            const int o = goff(I, decltype(q)::value);
+            static_for<NB>([&](auto j) EE_ALWAYS_INLINE { w[I % 2][decltype(q)::value][j] = raw4(wcol[j] + o); });
           });
-        });
-      }
+        }
+      };
+      load_w(std::integral_constant<int, 0>{});
       static_for<NPART>([&](auto hf) EE_ALWAYS_INLINE {
         constexpr int H = decltype(hf)::value, I0 = H * 2;
         __builtin_amdgcn_sched_barrier(0);
         float dg[32], db[32];
         static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
           constexpr int II = decltype(ii)::value, I = I0 + II;
+          load_w(std::integral_constant<int, I + 1>{});
           static_for<4>([&](auto q) EE_ALWAYS_INLINE {
             constexpr int Q = decltype(q)::value;
             const int o = goff(I, Q);
             const bool rok = kIn || rbase + I * 32 + Q * 8 < t.M;
-            const f32x4_t g4 = kG ? cvt4(raw4(p.gain + rbase + o)) : f32x4_t{1.0f, 1.0f, 1.0f, 1.0f};
-            const f32x4_t b4 = kB ? cvt4(raw4(p.bias + rbase + o)) : f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+            const int lo4 = rbase - t.m0 + o;  // tile row of the group (o clamped at the problem's edge)
+            const f32x4_t g4 = kG ? *reinterpret_cast<const f32x4_t *>(gl + lo4) : f32x4_t{1.0f, 1.0f, 1.0f, 1.0f};
+            const f32x4_t b4 = kB ? *reinterpret_cast<const f32x4_t *>(gl + Cfg::BM + lo4) : f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
             f32x4_t sg = {0.0f, 0.0f, 0.0f, 0.0f}, sb = {0.0f, 0.0f, 0.0f, 0.0f};
             static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
               const f32x4_t c = {acc[I][j][Q * 4], acc[I][j][Q * 4 + 1], acc[I][j][Q * 4 + 2], acc[I][j][Q * 4 + 3]};
@@ -356,7 +380,7 @@ struct EpiWeightGrad {
               if constexpr (kB) v += gs[j] * b4;
               if (cok[j] && rok) store4(dcol[j] + o, v);
               if constexpr (kW) {
-                const f32x4_t wv = cvt4(w[H][II][Q][j]);
+                const f32x4_t wv = cvt4(w[I % 2][Q][j]);
                 if (cok[j]) {
                   sg += wv * c;
                   if constexpr (kB) sb += wv * gs[j];
@@ -479,35 +503,6 @@ struct EpiSwiGLU {
   }
 };
 
-// Up projection with the SwiGLU product: H_u[n][i] = C[i][n],
-// A[n][i] = silu(H_g[n][i]) * H_u[n][i].
-template <typename T>
-struct EpiSwiGLUTr {
-  struct Params {
-    const T *Hg;
-    T *Hu;
-    T *A;
-    int64_t ld;
-  };
-  template <class Cfg>
-  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc4_loaded<Cfg>(
-        acc, t, [&](int row0, int col) EE_ALWAYS_INLINE { return load4(p.Hg + static_cast<int64_t>(col) * p.ld + row0); },
-        [&](int row0, int col, int, f32x4_t hu, f32x4_t hg) EE_ALWAYS_INLINE {
-          if (row0 < t.M && col < t.N) {
-            const int64_t o = static_cast<int64_t>(col) * p.ld + row0;
-            store4(p.Hu + o, hu);
-            f32x4_t a;
-            static_for<4>([&](auto e) EE_ALWAYS_INLINE {
-              constexpr int E = decltype(e)::value;
-              a[E] = silu_f(hg[E]) * hu[E];
-            });
-            store4(p.A + o, a);
-          }
-        });
-  }
-};
-
 // Down projection with the residual: Y[n][j] = X[n][j] + C[j][n]  (fp32 out).
 template <typename T>
 struct EpiResidualTr {
@@ -519,9 +514,9 @@ struct EpiResidualTr {
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
     for_each_acc4_loaded<Cfg>(
-        acc, t, [&](int row0, int col) EE_ALWAYS_INLINE { return load4(p.X + static_cast<int64_t>(col) * p.ld + row0); },
-        [&](int row0, int col, int, f32x4_t c, f32x4_t x) EE_ALWAYS_INLINE {
-          if (row0 < t.M && col < t.N) store4(p.Y + static_cast<int64_t>(col) * p.ld + row0, c + x);
+        acc, t, [&](int row0, int col) EE_ALWAYS_INLINE { return raw4(p.X + static_cast<int64_t>(col) * p.ld + row0); },
+        [&](int row0, int col, int, f32x4_t c, Raw4<T> x) EE_ALWAYS_INLINE {
+          if (row0 < t.M && col < t.N) store4(p.Y + static_cast<int64_t>(col) * p.ld + row0, c + cvt4(x));
         });
   }
 };
@@ -537,22 +532,28 @@ struct EpiSwiGLUBwdTr {
     T *dHu;
     int64_t ld;
   };
+  struct R2 {
+    Raw4<T> a, b;
+  };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
     for_each_acc4_loaded<Cfg>(
         acc, t,
         [&](int row0, int col) EE_ALWAYS_INLINE {
           const int64_t o = static_cast<int64_t>(col) * p.ld + row0;
-          return V2{load4(p.Hg + o), load4(p.Hu + o)};
+          return R2{raw4(p.Hg + o), raw4(p.Hu + o)};
         },
-        [&](int row0, int col, int, f32x4_t da, V2 h) EE_ALWAYS_INLINE {
+        [&](int row0, int col, int, f32x4_t da, R2 h) EE_ALWAYS_INLINE {
           if (row0 < t.M && col < t.N) {
             const int64_t o = static_cast<int64_t>(col) * p.ld + row0;
+            const f32x4_t hg = cvt4(h.a), hu = cvt4(h.b);
             f32x4_t dg, du;
             static_for<4>([&](auto e) EE_ALWAYS_INLINE {
               constexpr int E = decltype(e)::value;
-              dg[E] = da[E] * h.b[E] * silu_grad_f(h.a[E]);
-              du[E] = da[E] * silu_f(h.a[E]);
+              float sv, sg;
+              silu_and_grad(hg[E], sv, sg);
+              dg[E] = da[E] * hu[E] * sg;
+              du[E] = da[E] * sv;
             });
             store4(p.dHg + o, dg);
             store4(p.dHu + o, du);
