@@ -48,6 +48,7 @@ struct Layout {
          dgpg = 0, dgpu = 0;
   size_t mu = 0, gsp = 0, gsum = 0, dbp = 0;  // LayerNorm mean; bias: G row sums, bias partials
   int dzs = 1;                                // split-K slices of the dZ product
+  ee::DownSplit ys{0, 0, 1};                  // split-K tail of the down projection
   int64_t gchunks = 0;
   size_t total = 0;
 };
@@ -99,7 +100,8 @@ Layout layout(const ee_exit &e, int64_t n) {
     L.hg = take(N * I * es);
     L.hu = take(N * I * es);
     L.act = take(N * I * es);
-    L.y = take(N * h * 4);
+    L.ys = ee::down_split(f32, static_cast<int>(n), static_cast<int>(h), static_cast<int>(I));
+    L.y = take(static_cast<size_t>(L.ys.splits) * N * h * 4);
     L.dzs = ee::dz_splits(f32, static_cast<int>(L.ldn), static_cast<int>(h), static_cast<int>(V));
     L.dz = take(static_cast<size_t>(L.dzs) * N * h * 4);
     L.dy = take(N * h * es);
@@ -306,8 +308,8 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
                                  at(ws, L.uhat), nullptr, s));
     EE_LAUNCH("gate projection", s, ee::gemm_gate(f32, at(ws, L.u), e.w_gate, n, I, h, at(ws, L.hg), s));
     EE_LAUNCH("up projection + swiglu", s, ee::gemm_up_swiglu(f32, at(ws, L.u), e.w_up, n, I, h, at(ws, L.hg), at(ws, L.hu), at(ws, L.act), s));
-    EE_LAUNCH("down projection + residual", s, ee::gemm_down_residual(f32, at(ws, L.act), e.w_down, x, n, h, I, atf(ws, L.y), s));
-    EE_LAUNCH("exit norm rms", s, ee::launch_row_rms(true, atf(ws, L.y), h, n, h, e.rms_eps, atf(ws, L.r), s));
+    EE_LAUNCH("down projection + residual", s, ee::gemm_down_residual(f32, at(ws, L.act), e.w_down, x, n, h, I, atf(ws, L.y), s, L.ys));
+    EE_LAUNCH("exit norm rms", s, ee::launch_row_rms_split(atf(ws, L.y), n, h, e.rms_eps, atf(ws, L.r), L.ys, s));
     EE_LAUNCH("exit norm apply", s, ee::launch_norm_apply(true, f32, atf(ws, L.y), h, atf(ws, L.r), e.gamma, n, ldn, h, at(ws, L.z),
                                  nullptr, at(ws, L.zht), s));
     zsrc = at(ws, L.z);

@@ -504,20 +504,32 @@ struct EpiSwiGLU {
 };
 
 // Down projection with the residual: Y[n][j] = X[n][j] + C[j][n]  (fp32 out).
+// With split K, slice z of the product goes to Y + z * zstride and only
+// slice 0 adds X (the slices are partial sums the exit-norm statistics add).
 template <typename T>
 struct EpiResidualTr {
   struct Params {
     float *Y;       // [N][ld]
     const T *X;     // [N][ld]
     int64_t ld;
+    int64_t zstride;
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc4_loaded<Cfg>(
-        acc, t, [&](int row0, int col) EE_ALWAYS_INLINE { return raw4(p.X + static_cast<int64_t>(col) * p.ld + row0); },
-        [&](int row0, int col, int, f32x4_t c, Raw4<T> x) EE_ALWAYS_INLINE {
-          if (row0 < t.M && col < t.N) store4(p.Y + static_cast<int64_t>(col) * p.ld + row0, c + cvt4(x));
-        });
+    float *Y = p.Y + t.kz * p.zstride;
+    if (t.kz == 0) {
+      for_each_acc4_loaded<Cfg>(
+          acc, t, [&](int row0, int col) EE_ALWAYS_INLINE { return raw4(p.X + static_cast<int64_t>(col) * p.ld + row0); },
+          [&](int row0, int col, int, f32x4_t c, Raw4<T> x) EE_ALWAYS_INLINE {
+            if (row0 < t.M && col < t.N) store4(Y + static_cast<int64_t>(col) * p.ld + row0, c + cvt4(x));
+          });
+    } else {
+      for_each_acc4_loaded<Cfg>(
+          acc, t, [&](int, int) EE_ALWAYS_INLINE { return 0; },
+          [&](int row0, int col, int, f32x4_t c, int) EE_ALWAYS_INLINE {
+            if (row0 < t.M && col < t.N) store4(Y + static_cast<int64_t>(col) * p.ld + row0, c);
+          });
+    }
   }
 };
 

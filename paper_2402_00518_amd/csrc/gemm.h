@@ -527,7 +527,8 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
 // multiple of 8 (the blocks in between do nothing), so that both keep the
 // XCD-aware tile order.  The hardware dispatches blocks in order, so the
 // problems share the GPU only where the first one's last round of tiles
-// leaves CUs idle.  No split K.
+// leaves CUs idle.  Problem 2 may be split along K (s2.kchunk > 0): its
+// blocks then run slice by slice, each slice over all of its tiles.
 template <typename T, bool AK1, bool BKM1, class Epi1, bool AK2, bool BKM2, class Epi2, class Cfg>
 __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_pair_kernel(
     Operand A1, Operand B1, GemmShape s1, typename Epi1::Params ep1, Operand A2, Operand B2, GemmShape s2,
@@ -536,8 +537,10 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_pair_kerne
   const int b = blockIdx.x;
   if (b < blocks1)
     gemm_block<T, AK1, BKM1, Epi1, Cfg>(A1, B1, s1, ep1, b, blocks1, 0, smem);
-  else if (b >= base2)
-    gemm_block<T, AK2, BKM2, Epi2, Cfg>(A2, B2, s2, ep2, b - base2, gridDim.x - base2, 0, smem);
+  else if (b >= base2) {
+    const int tiles2 = cdiv(s2.M, Cfg::BM) * cdiv(s2.N, Cfg::BN), b2 = b - base2;
+    gemm_block<T, AK2, BKM2, Epi2, Cfg>(A2, B2, s2, ep2, b2 % tiles2, tiles2, b2 / tiles2, smem);
+  }
 }
 
 // Shapes the loaders handle.
@@ -571,14 +574,20 @@ hipError_t launch_gemm_pair(Operand A1, Operand B1, GemmShape s1, const typename
                             Operand B2, GemmShape s2, const typename Epi2::Params &ep2, hipStream_t stream) {
   const int64_t b1 = static_cast<int64_t>(cdiv(s1.M, Cfg::BM)) * cdiv(s1.N, Cfg::BN);
   const int64_t b2 = static_cast<int64_t>(cdiv(s2.M, Cfg::BM)) * cdiv(s2.N, Cfg::BN);
-  if (s1.kchunk != 0 || s2.kchunk != 0) return hipErrorInvalidValue;
+  constexpr int BK = 8 * Elem<T>::CH;
+  if (s1.kchunk != 0) return hipErrorInvalidValue;
   if (b1 <= 0) return launch_gemm<T, AK2, BKM2, Epi2, Cfg>(A2, B2, s2, ep2, stream);
   if (b2 <= 0) return launch_gemm<T, AK1, BKM1, Epi1, Cfg>(A1, B1, s1, ep1, stream);
   if (!gemm_shape_ok<T, AK1, BKM1>(A1, B1, s1) || !gemm_shape_ok<T, AK2, BKM2>(A2, B2, s2))
     return hipErrorInvalidValue;
+  int64_t splits2 = 1;
+  if (s2.kchunk > 0) {
+    if (s2.kchunk % BK != 0) return hipErrorInvalidValue;
+    splits2 = cdiv(s2.K, s2.kchunk);
+  }
   const int64_t base2 = (b1 + kNumXcd - 1) / kNumXcd * kNumXcd;
   hipLaunchKernelGGL((gemm_pair_kernel<T, AK1, BKM1, Epi1, AK2, BKM2, Epi2, Cfg>),
-                     dim3(static_cast<unsigned>(base2 + b2)), dim3(Cfg::THREADS), 0, stream, A1, B1, s1, ep1, A2,
+                     dim3(static_cast<unsigned>(base2 + b2 * splits2)), dim3(Cfg::THREADS), 0, stream, A1, B1, s1, ep1, A2,
                      B2, s2, ep2, static_cast<int>(b1), static_cast<int>(base2));
   return hipGetLastError();
 }

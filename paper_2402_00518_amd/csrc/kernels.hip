@@ -3,7 +3,11 @@
 // instantiations with their fused epilogues.
 #include <math.h>
 
+#include <algorithm>
+#include <functional>
+#include <queue>
 #include <type_traits>
+#include <vector>
 
 #include "epilogues.h"
 #include "launch.h"
@@ -104,6 +108,52 @@ __global__ __launch_bounds__(256) void row_rms_kernel(const Tin *x, int64_t ldx,
     r[row] = 1.0f / sqrtf(s / static_cast<float>(h) + eps);
     if (mu != nullptr) mu[row] = mean;
   }
+}
+
+// RMSNorm statistics of the fp32 rows the split down projection leaves:
+// outputs of tokens >= tok0 and features >= feat0 are held as SL partial
+// sums zstride floats apart, which are first added up in slice order and
+// the sum written over slice 0.  One wave per row; each lane rewrites only
+// the elements it reads, and issues the loads of four 256-float groups
+// before it adds and stores.
+template <int SL>
+__global__ __launch_bounds__(256) void row_rms_split_kernel(float *x, int n, int h, float eps, float *r, int tok0,
+                                                            int feat0, int64_t zstride) {
+  constexpr int U = 4, G = kWave * 4;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= n) return;
+  float *xr = x + static_cast<int64_t>(row) * h;
+  const int f0 = row >= tok0 ? feat0 : h;  // features from f0 on are split
+  float s = 0.0f;
+  for (int j0 = lane * 4; j0 < h; j0 += U * G) {
+    f32x4_t v[U][SL];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * G;
+      if (j < h) {
+        v[u][0] = load4(xr + j);
+        if (j >= f0) {
+#pragma unroll
+          for (int z = 1; z < SL; ++z) v[u][z] = load4(xr + z * zstride + j);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * G;
+      if (j < h) {
+        f32x4_t a = v[u][0];
+        if (j >= f0) {
+#pragma unroll
+          for (int z = 1; z < SL; ++z) a += v[u][z];
+          store4(xr + j, a);
+        }
+        s += a[0] * a[0] + a[1] * a[1] + a[2] * a[2] + a[3] * a[3];
+      }
+    }
+  }
+  s = warp_sum(s);
+  if (lane == 0) r[row] = 1.0f / sqrtf(s / static_cast<float>(h) + eps);
 }
 
 // 64 tokens x 64 features per block.  Row-major outputs are written
@@ -469,6 +519,27 @@ hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, 
   return hipGetLastError();
 }
 
+hipError_t launch_row_rms_split(float *x, int n, int h, float eps, float *r, DownSplit sp, hipStream_t stream) {
+  if (sp.splits <= 1) return launch_row_rms(true, x, h, n, h, eps, r, stream);
+  if (h % 4 != 0 || sp.tok0 < 0 || sp.tok0 > n || sp.feat0 < 0 || sp.feat0 > h) return hipErrorInvalidValue;
+  const dim3 grid(cdiv(n, 4));
+  const int64_t zs = static_cast<int64_t>(n) * h;
+  switch (sp.splits) {
+    case 2:
+      hipLaunchKernelGGL(row_rms_split_kernel<2>, grid, dim3(256), 0, stream, x, n, h, eps, r, sp.tok0, sp.feat0, zs);
+      break;
+    case 3:
+      hipLaunchKernelGGL(row_rms_split_kernel<3>, grid, dim3(256), 0, stream, x, n, h, eps, r, sp.tok0, sp.feat0, zs);
+      break;
+    case 4:
+      hipLaunchKernelGGL(row_rms_split_kernel<4>, grid, dim3(256), 0, stream, x, n, h, eps, r, sp.tok0, sp.feat0, zs);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, const float *r,
                              const void *gain, int n, int ldn, int h, void *z, void *x_hat, void *x_hat_t,
                              hipStream_t stream, const float *mu, const void *bias) {
@@ -622,13 +693,101 @@ hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int 
 }
 
 hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, const void *x, int n, int h,
-                              int inter, float *y, hipStream_t stream) {
+                              int inter, float *y, hipStream_t stream, DownSplit sp) {
   EE_DISPATCH(f32, {
-    typename EpiResidualTr<T>::Params ep{y, static_cast<const T *>(x), h};
-    return run_gemm<T, true, true, EpiResidualTr<T>>(Operand{w_down, inter}, Operand{act, inter},
-                                                        GemmShape{h, n, inter}, ep, stream);
+    const T *xt = static_cast<const T *>(x), *at = static_cast<const T *>(act), *wd = static_cast<const T *>(w_down);
+    // Split region: tokens [t0, n) x features [f0, h).  The rest takes all of
+    // K: tokens [0, t0) (f0 == 0) or features [0, f0) (t0 == 0).
+    const bool split = sp.splits > 1;
+    const int t0 = split ? sp.tok0 : n, f0 = split ? sp.feat0 : 0;
+    if (t0 < 0 || t0 > n || f0 < 0 || f0 > h || (t0 > 0 && f0 > 0)) return hipErrorInvalidValue;
+    const int m1 = t0 > 0 ? h : f0, n1 = t0 > 0 ? t0 : n;
+    const int64_t o = static_cast<int64_t>(t0) * h + f0;
+    typename EpiResidualTr<T>::Params e1{y, xt, h, 0};
+    typename EpiResidualTr<T>::Params e2{y + o, xt + o, h, static_cast<int64_t>(n) * h};
+    GemmShape s2{h - f0, n - t0, inter};
+    if (split) {
+      s2.kchunk = split_kchunk(inter, sp.splits);
+      if (cdiv(inter, s2.kchunk) != sp.splits) return hipErrorInvalidValue;  // Y holds sp.splits slices
+    }
+    return run_gemm_pair<T, true, true, EpiResidualTr<T>, true, true, EpiResidualTr<T>>(
+        Operand{wd, inter}, Operand{at, inter}, GemmShape{m1, n1, inter}, e1,
+        Operand{wd + static_cast<int64_t>(f0) * inter, inter}, Operand{at + static_cast<int64_t>(t0) * inter, inter},
+        s2, e2, stream);
   });
   return hipSuccess;
+}
+
+namespace {
+
+constexpr int kCus = 256;           // compute units the launch shapes are planned for
+constexpr double kEpilogueK = 1024;  // prologue and epilogue of a 256 x 256 tile, in K values of its main loop
+constexpr double kBytesPerK = 1.2e5;  // HBM bytes moved while a CU runs one such K value
+
+// Duration, in K values, of `full` whole-K tiles followed by `parts` blocks
+// of kchunk K values each, dispatched in order to the first free of kCus
+// compute units.
+double launch_span(int64_t full, int64_t parts, int K, int kchunk) {
+  const double D = K + kEpilogueK, d = kchunk + kEpilogueK;
+  const int64_t rest = full % kCus;
+  std::priority_queue<double, std::vector<double>, std::greater<double>> q;
+  double end = rest > 0 ? D : 0.0;
+  for (int i = 0; i < kCus; ++i) q.push(i < rest ? D : 0.0);
+  for (int64_t p = 0; p < parts; ++p) {
+    const double t = q.top() + d;
+    q.pop();
+    q.push(t);
+    end = std::max(end, t);
+  }
+  return static_cast<double>(full / kCus) * D + end;
+}
+
+}  // namespace
+
+int split_kchunk(int K, int splits) { return cdiv(cdiv(K, splits), 64) * 64; }
+
+DownSplit down_split(bool f32, int n, int h, int inter) {
+  DownSplit best{n, 0, 1};
+  if (f32 || n <= 0) return best;
+  static thread_local int key[3] = {-1, -1, -1};
+  static thread_local DownSplit memo{0, 0, 1};
+  if (key[0] == n && key[1] == h && key[2] == inter) return memo;
+  const int tm = cdiv(h, CfgBig::BM), tn = cdiv(n, CfgBig::BN);
+  const int64_t tiles = static_cast<int64_t>(tm) * tn;
+  if (tiles < 4 * kCus) {
+    const int64_t rounds = tiles / kCus;
+    double best_span = 0.9 * launch_span(tiles, 0, inter, inter);
+    for (int s = 2; s <= 4; s *= 2) {
+      if (inter / s < 4 * 64) break;
+      const int kc = split_kchunk(inter, s), slices = cdiv(inter, kc);
+      // Split the last c token blocks (dim 0) or feature blocks (dim 1):
+      // all of them, or the fewest that leave the whole-K tiles one or two
+      // rounds short of the current count.
+      for (int dim = 0; dim < 2; ++dim) {
+        const int blocks = dim == 0 ? tn : tm, across = dim == 0 ? tm : tn;
+        int cand[3] = {blocks, 0, 0};
+        for (int r = 0; r < 2; ++r)
+          if (rounds - r >= 0) cand[r + 1] = static_cast<int>((tiles - (rounds - r) * kCus + across - 1) / across);
+        for (int c : cand) {
+          if (c < 1 || c > blocks) continue;
+          const DownSplit sp = dim == 0 ? DownSplit{(tn - c) * CfgBig::BN, 0, slices}
+                                        : DownSplit{0, (tm - c) * CfgBig::BM, slices};
+          // extra HBM traffic: slices 1.. written and read back, their sum written
+          const double outs = static_cast<double>(n - sp.tok0) * (h - sp.feat0);
+          const double extra = outs * 4 * (2 * (slices - 1) + 1) / kBytesPerK;
+          const double span = launch_span(static_cast<int64_t>(blocks - c) * across,
+                                          static_cast<int64_t>(c) * across * slices, inter, kc) + extra;
+          if (span < best_span) {
+            best_span = span;
+            best = sp;
+          }
+        }
+      }
+    }
+  }
+  key[0] = n, key[1] = h, key[2] = inter;
+  memo = best;
+  return best;
 }
 
 int dz_splits(bool f32, int ldn, int h, int vocab) {
@@ -639,17 +798,15 @@ int dz_splits(bool f32, int ldn, int h, int vocab) {
   const int tiles = cdiv(ldn, CfgBig::BM) * cdiv(h, CfgBig::BN);
   int s = 1;
   while (s < 4 && tiles * s < 1024 && vocab / (2 * s) >= 4 * 64) s *= 2;
-  return cdiv(vocab, dz_kchunk(vocab, s));
+  return cdiv(vocab, split_kchunk(vocab, s));
 }
-
-int dz_kchunk(int vocab, int splits) { return cdiv(cdiv(vocab, splits), 64) * 64; }
 
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab, float *dz,
                    hipStream_t stream, int splits) {
   EE_DISPATCH(f32, {
     typename EpiStoreF32<T>::Params ep{dz, h, n, 0, static_cast<int64_t>(n) * h};
     GemmShape sh{ldn, h, vocab};
-    if (splits > 1) sh.kchunk = dz_kchunk(vocab, splits);
+    if (splits > 1) sh.kchunk = split_kchunk(vocab, splits);
     return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{g_t, ldn}, Operand{w_out, h}, sh, ep, stream);
   });
   return hipSuccess;

@@ -10,6 +10,15 @@ namespace ee {
 
 constexpr int kTokenPad = 64;     // padding of the token dimension
 
+// Split-K tail of the MLP exit's down projection (gemm_down_residual): the
+// outputs of tokens >= tok0 and features >= feat0 (one of the two is 0) are
+// computed as `splits` partial sums over slices of K; the rest take all of K.
+struct DownSplit {
+  int tok0;
+  int feat0;
+  int splits;  // 1: no split
+};
+
 // Width of the column slices over which the logits and weight-gradient
 // GEMMs keep their softmax and gain-gradient partials (one wave's columns).
 int gemm_part_cols(bool f32);
@@ -19,6 +28,10 @@ int gemm_part_cols(bool f32);
 // r[n] = (mean_j (x[n][j] - mu[n])^2 + eps)^(-1/2).
 hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps,
                           float *r, hipStream_t stream, float *mu = nullptr);
+// RMSNorm statistics of the fp32 rows the split down projection leaves
+// (see gemm_down_residual): the split outputs are first replaced by the sum
+// of their slices, in slice order.
+hipError_t launch_row_rms_split(float *x, int n, int h, float eps, float *r, DownSplit sp, hipStream_t stream);
 
 // Apply the row statistics, a gain and a bias: x_hat = (x - mu[n]) * r[n]
 // (mu == NULL: no centring; r == NULL: no scale), z = x_hat * gain + bias
@@ -98,14 +111,20 @@ hipError_t gemm_gate(bool f32, const void *u, const void *w_gate, int n, int int
 // H_u = U W_up^T, A = silu(H_g) H_u.
 hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int inter, int h,
                           const void *hg, void *hu, void *act, hipStream_t stream);
-// Y[n][h] = X + A W_down^T  (fp32 out).
+// K values per slice when a product of depth K runs as `splits` partial sums.
+int split_kchunk(int K, int splits);
+// Y[n][h] = X + A W_down^T  (fp32 out).  With sp.splits > 1 the outputs in
+// sp's region are sp.splits partial sums over slices of I: slice 0 (which
+// adds X) in place, slice z at Y + z n h, so Y holds splits n h floats;
+// launch_row_rms_split with the same split adds them up.  down_split: the
+// split for a shape.
+DownSplit down_split(bool f32, int n, int h, int inter);
 hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, const void *x, int n,
-                              int h, int inter, float *y, hipStream_t stream);
+                              int h, int inter, float *y, hipStream_t stream, DownSplit sp = DownSplit{0, 0, 1});
 // dZ[n][h] = G W_out with G stored transposed [V][ldn]  (fp32 out), as
 // `splits` partial sums over slices of the vocabulary, n*h floats apart
 // (dz_splits: the count for a shape; the buffer holds that many slices).
 int dz_splits(bool f32, int ldn, int h, int vocab);
-int dz_kchunk(int vocab, int splits);
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab,
                    float *dz, hipStream_t stream, int splits = 1);
 // One launch of two independent products of the MLP backward:

@@ -116,6 +116,12 @@ SMALL_CASES = [
     # M of dW_out), and 8192 for an MLP exit (the norm backward's limit)
     ("norm_max_hidden", W.EXIT_NORM, 40, 32768, 200, 0, "bf16", False),
     ("mlp_max_hidden", W.EXIT_MLP, 96, 8192, 300, 256, "bf16", False),
+    # the down projection with a split-K tail: 256 whole-K tiles (tokens
+    # 0-2047) plus the last 152 tokens as four partial sums over I; then
+    # features 0-5375 whole and the last 64 features of every token as four
+    # partial sums over a ragged I (mlp_multi_tile: all outputs as two)
+    ("mlp_split_tokens", W.EXIT_MLP, 2200, 8192, 300, 1024, "bf16", False),
+    ("mlp_split_features", W.EXIT_MLP, 3000, 5440, 300, 1088, "bf16", False),
 ]
 
 
