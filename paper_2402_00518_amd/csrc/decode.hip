@@ -3,15 +3,17 @@
 //
 // At decode the products are skinny, C[r][j] = sum_k W[r][k] Z[j][k] with
 // a weight W of R rows and only B <= 32 token rows Z per pass, so they are
-// bound by streaming W from HBM once.  A block of four waves owns 32 rows of
-// W; each wave takes a quarter of K and reads its rows straight into MFMA A
-// fragments (16 bytes of K per lane), 8 fragments in flight per lane per
-// group, with no LDS staging; the token rows come from L2 as B fragments
-// (tokens past B re-read row B-1 and their outputs are dropped).  The four
-// partial sums meet in LDS in a fixed order and the first wave runs the
-// epilogue.  Splitting K gives about 4000 waves at V = 32000, enough loads in
-// flight on every CU.  bf16 uses v_mfma_f32_32x32x16_bf16, fp32
-// v_mfma_f32_32x32x2_f32 over the same 16-byte loads.
+// bound by streaming W from HBM once.  A block owns 32 rows of W (64 for
+// a wide W past 8 token rows, so that each token fragment serves two row
+// groups and the token rows' share of the loads halves); each of its waves takes a share
+// of K and reads its rows straight into MFMA A fragments (16 bytes of K per
+// lane), 8 fragments per row group in flight per lane, with no LDS staging;
+// the token rows come from L2 as B fragments (tokens past B re-read row B-1
+// and their outputs are dropped).  The waves' partial sums meet in LDS in a
+// fixed order and the first wave runs the epilogue.  Splitting K gives about
+// 4000 waves at V = 32000, enough loads in flight on every CU.  bf16 uses
+// v_mfma_f32_32x32x16_bf16, fp32 v_mfma_f32_32x32x2_f32 over the same
+// 16-byte loads.
 //
 // Epilogues: store (gate projection), SwiGLU (up projection), residual
 // (down projection) and, for the output matrix, per-wave softmax partials:
@@ -20,6 +22,8 @@
 // of all waves into the greedy token, its probability and the exit flag.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "ee_device.h"
 #include "launch.h"
 
@@ -27,7 +31,7 @@ namespace ee {
 
 namespace {
 
-constexpr int kDecRows = 32;    // rows of W per block
+constexpr int kDecRows = 32;    // rows of W per row group (one MFMA tile)
 constexpr int kDecTokens = 32;  // token rows per pass (grid.y walks more)
 // Waves per block (each a share of K): 4 when the rows give at least two
 // blocks per CU of a 256-CU GPU, else 8 or 16, so that narrow products (the
@@ -65,7 +69,7 @@ __device__ __forceinline__ int dec_row(int r0, int lane, int v) {
   return r0 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
 }
 
-template <typename T, class Epi, int kDecWaves>
+template <typename T, class Epi, int kDecWaves, int RG>
 __global__ __launch_bounds__(64 * kDecWaves) void skinny_kernel(const T *__restrict__ W, int64_t ldw, int R,
                                                                 const T *__restrict__ Z, int64_t ldz, int B, int K,
                                                                 typename Epi::Params ep) {
@@ -73,52 +77,65 @@ __global__ __launch_bounds__(64 * kDecWaves) void skinny_kernel(const T *__restr
   constexpr int PER_LOAD = 16 / sizeof(T);  // elements of one 16-byte load
   __shared__ f32x16_t red[kDecWaves - 1][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r0 = blockIdx.x * kDecRows, j0 = blockIdx.y * kDecTokens;
-  const int wr = min(r0 + (lane & 31), R - 1);
+  const int r0 = blockIdx.x * kDecRows * RG, j0 = blockIdx.y * kDecTokens;
   const int zr = min(j0 + (lane & 31), B - 1);
   const int koff = (lane >> 5) * PER_LOAD;
-  const char *wp = reinterpret_cast<const char *>(W + static_cast<int64_t>(wr) * ldw + koff);
+  const char *wp[RG];
+  static_for<RG>([&](auto g) EE_ALWAYS_INLINE {
+    constexpr int G = decltype(g)::value;
+    const int wr = min(r0 + G * kDecRows + (lane & 31), R - 1);
+    wp[G] = reinterpret_cast<const char *>(W + static_cast<int64_t>(wr) * ldw + koff);
+  });
   const char *zp = reinterpret_cast<const char *>(Z + static_cast<int64_t>(zr) * ldz + koff);
-  f32x16_t acc;
-  static_for<16>([&](auto v) EE_ALWAYS_INLINE { acc[decltype(v)::value] = 0.0f; });
+  f32x16_t acc[RG];
+  static_for<RG>([&](auto g) EE_ALWAYS_INLINE {
+    static_for<16>([&](auto v) EE_ALWAYS_INLINE { acc[decltype(g)::value][decltype(v)::value] = 0.0f; });
+  });
 
   // This wave's share of K, in whole groups of 4 loads (K is a multiple of
-  // 4 KL): groups [g0, g1) of the K / (4 KL) groups.
+  // 4 KL): groups [g0, g1) of the K / (4 KL) groups.  Each token fragment
+  // serves the RG row groups of the block.
   constexpr int KG4 = 4 * KL;
   const int groups = K / KG4;
   const int g0 = wave * groups / kDecWaves, g1 = (wave + 1) * groups / kDecWaves;
   int k = g0 * KG4;
   const int kend = g1 * KG4;
-  constexpr int KG = kDecGroup * KL;
-  for (; k + KG <= kend; k += KG) {
-    u32x4_t a[kDecGroup], b[kDecGroup];
-    static_for<kDecGroup>([&](auto q) EE_ALWAYS_INLINE {
+  auto step = [&](auto nq) EE_ALWAYS_INLINE {
+    constexpr int NQ = decltype(nq)::value;
+    u32x4_t a[RG][NQ], b[NQ];
+    static_for<NQ>([&](auto q) EE_ALWAYS_INLINE {
       constexpr int Q = decltype(q)::value;
-      a[Q] = *reinterpret_cast<const u32x4_t *>(wp + (static_cast<int64_t>(k) + Q * KL) * sizeof(T));
-      b[Q] = *reinterpret_cast<const u32x4_t *>(zp + (static_cast<int64_t>(k) + Q * KL) * sizeof(T));
+      const int64_t off = (static_cast<int64_t>(k) + Q * KL) * sizeof(T);
+      static_for<RG>([&](auto g) EE_ALWAYS_INLINE {
+        a[decltype(g)::value][Q] = *reinterpret_cast<const u32x4_t *>(wp[decltype(g)::value] + off);
+      });
+      b[Q] = *reinterpret_cast<const u32x4_t *>(zp + off);
     });
     // Keep every load of the group ahead of the MFMAs: left alone, the
     // scheduler would trade loads in flight for registers.
     __builtin_amdgcn_sched_barrier(0);
-    static_for<kDecGroup>([&](auto q) EE_ALWAYS_INLINE { DecFrag<T>::mma(a[decltype(q)::value], b[decltype(q)::value], acc); });
-  }
-  for (; k < kend; k += KG4) {
-    u32x4_t a[4], b[4];
-    static_for<4>([&](auto q) EE_ALWAYS_INLINE {
-      constexpr int Q = decltype(q)::value;
-      a[Q] = *reinterpret_cast<const u32x4_t *>(wp + (static_cast<int64_t>(k) + Q * KL) * sizeof(T));
-      b[Q] = *reinterpret_cast<const u32x4_t *>(zp + (static_cast<int64_t>(k) + Q * KL) * sizeof(T));
+    static_for<NQ>([&](auto q) EE_ALWAYS_INLINE {
+      static_for<RG>([&](auto g) EE_ALWAYS_INLINE {
+        DecFrag<T>::mma(a[decltype(g)::value][decltype(q)::value], b[decltype(q)::value], acc[decltype(g)::value]);
+      });
     });
-    __builtin_amdgcn_sched_barrier(0);
-    static_for<4>([&](auto q) EE_ALWAYS_INLINE { DecFrag<T>::mma(a[decltype(q)::value], b[decltype(q)::value], acc); });
-  }
-  // Partial sums of waves 1..3 to LDS; wave 0 adds them in order and
-  // finishes.
-  if (wave > 0) red[wave - 1][lane] = acc;
-  __syncthreads();
-  if (wave != 0) return;
-  static_for<kDecWaves - 1>([&](auto w) EE_ALWAYS_INLINE { acc += red[decltype(w)::value][lane]; });
-  Epi::apply(ep, acc, r0, j0, lane, R, B);
+  };
+  constexpr int KG = kDecGroup * KL;
+  for (; k + KG <= kend; k += KG) step(std::integral_constant<int, kDecGroup>{});
+  for (; k < kend; k += KG4) step(std::integral_constant<int, 4>{});
+  // Per row group: partial sums of waves 1.. to LDS; wave 0 adds them in
+  // order and finishes.
+  static_for<RG>([&](auto g) EE_ALWAYS_INLINE {
+    constexpr int G = decltype(g)::value;
+    if (G > 0) __syncthreads();  // wave 0 has read the previous group
+    if (wave > 0) red[wave - 1][lane] = acc[G];
+    __syncthreads();
+    if (wave == 0 && r0 + G * kDecRows < R) {  // a second group may lie past the last row
+      f32x16_t c = acc[G];
+      static_for<kDecWaves - 1>([&](auto w) EE_ALWAYS_INLINE { c += red[decltype(w)::value][lane]; });
+      Epi::apply(ep, c, r0 + G * kDecRows, j0, lane, R, B);
+    }
+  });
 }
 
 // Four consecutive rows of one token as fp32 (bf16 or fp32 storage).
@@ -207,9 +224,9 @@ struct DecResidual {  // Y[j][r] = X[j][r] + C[r][j]  (fp32 out)
   }
 };
 
-// Softmax partials of the output-matrix product over the wave's 32 rows
-// (vocabulary ids), per token: m = max, arg = lowest id reaching m,
-// l = sum exp(S - m).  Stored at [wave tile][token].
+// Softmax partials of the output-matrix product over 32 rows (vocabulary
+// ids), per token: m = max, arg = lowest id reaching m, l = sum exp(S - m).
+// Stored at [32-row tile][token].
 struct DecLogits {
   struct Params {
     float *part_m;
@@ -244,7 +261,7 @@ struct DecLogits {
     l += __shfl_xor(l, 32);
     const int j = j0 + lane;
     if (lane < 32 && j < B) {
-      const int64_t o = static_cast<int64_t>(blockIdx.x) * p.ld + j;
+      const int64_t o = static_cast<int64_t>(r0 / kDecRows) * p.ld + j;
       p.part_m[o] = m;
       p.part_l[o] = l;
       p.part_arg[o] = arg;
@@ -307,27 +324,41 @@ __global__ __launch_bounds__(256) void decide_kernel(const float *part_m, const 
   }
 }
 
+template <typename T, class Epi, int RG>
+hipError_t launch_skinny_rg(const T *w, int64_t ldw, int R, const T *z, int64_t ldz, int B, int K,
+                            const typename Epi::Params &ep, hipStream_t stream) {
+  const int row_blocks = (R + kDecRows * RG - 1) / (kDecRows * RG);
+  const dim3 grid(static_cast<unsigned>(row_blocks), static_cast<unsigned>((B + kDecTokens - 1) / kDecTokens));
+  // 16 waves of 1024 threads leave 128 registers a lane: too few for two row groups
+  const int waves = RG > 1 ? std::min(dec_waves(row_blocks), 8) : dec_waves(row_blocks);
+  switch (waves) {
+    case 4:
+      hipLaunchKernelGGL((skinny_kernel<T, Epi, 4, RG>), grid, dim3(64 * 4), 0, stream, w, ldw, R, z, ldz, B, K, ep);
+      break;
+    case 8:
+      hipLaunchKernelGGL((skinny_kernel<T, Epi, 8, RG>), grid, dim3(64 * 8), 0, stream, w, ldw, R, z, ldz, B, K, ep);
+      break;
+    default:
+      if constexpr (RG == 1)
+        hipLaunchKernelGGL((skinny_kernel<T, Epi, kDecWavesMax, RG>), grid, dim3(64 * kDecWavesMax), 0, stream, w, ldw,
+                           R, z, ldz, B, K, ep);
+  }
+  return hipGetLastError();
+}
+
+// Past 8 token rows, a wide W (at least 12288 rows) is read by blocks of two
+// 32-row groups per token fragment, halving the token rows' share of the
+// loads (at 8 waves a block: measured 11% faster at 32 tokens for 13824 and
+// 32000 rows; with 5120 rows the 80 blocks kept too few loads in flight).
 template <typename T, class Epi>
 hipError_t launch_skinny(const void *W, int64_t ldw, int R, const void *Z, int64_t ldz, int B, int K,
                          const typename Epi::Params &ep, hipStream_t stream) {
   if (R <= 0 || B <= 0) return hipSuccess;
   if (K % (4 * DecFrag<T>::K_PER_LOAD) != 0) return hipErrorInvalidValue;
-  const int row_blocks = (R + kDecRows - 1) / kDecRows;
-  const dim3 grid(static_cast<unsigned>(row_blocks), static_cast<unsigned>((B + kDecTokens - 1) / kDecTokens));
   const T *w = static_cast<const T *>(W);
   const T *z = static_cast<const T *>(Z);
-  switch (dec_waves(row_blocks)) {
-    case 4:
-      hipLaunchKernelGGL((skinny_kernel<T, Epi, 4>), grid, dim3(64 * 4), 0, stream, w, ldw, R, z, ldz, B, K, ep);
-      break;
-    case 8:
-      hipLaunchKernelGGL((skinny_kernel<T, Epi, 8>), grid, dim3(64 * 8), 0, stream, w, ldw, R, z, ldz, B, K, ep);
-      break;
-    default:
-      hipLaunchKernelGGL((skinny_kernel<T, Epi, kDecWavesMax>), grid, dim3(64 * kDecWavesMax), 0, stream, w, ldw, R,
-                         z, ldz, B, K, ep);
-  }
-  return hipGetLastError();
+  if (B > 8 && R >= 12288) return launch_skinny_rg<T, Epi, 2>(w, ldw, R, z, ldz, B, K, ep, stream);
+  return launch_skinny_rg<T, Epi, 1>(w, ldw, R, z, ldz, B, K, ep, stream);
 }
 
 }  // namespace

@@ -111,6 +111,11 @@ CASES = [
     ("layernorm_bias_f32", W.EXIT_NORM, 4, 64, 333, 0, "f32"),
     ("norm_max_hidden", W.EXIT_NORM, 3, 32768, 500, 0, "bf16"),
     ("mlp_max_hidden", W.EXIT_MLP, 5, 8192, 300, 256, "bf16"),
+    # past 8 rows a weight of at least 12288 rows is read 64 rows a block:
+    # the last block's second 32-row group lies past the vocabulary
+    ("norm_wide_vocab", W.EXIT_NORM, 20, 128, 12300, 0, "bf16"),
+    ("norm_wide_vocab_f32", W.EXIT_NORM, 12, 64, 12320, 0, "f32"),
+    ("mlp_wide_inter", W.EXIT_MLP, 40, 128, 500, 12352, "bf16"),
 ]
 
 
