@@ -424,7 +424,7 @@ ee_status check_aliasing(int n_exits, const ee_exit *exits, const void *const *h
 // ------------------------------------------------------------ decode
 // Workspace regions of the decode-time decision for n rows.
 struct DecLayout {
-  size_t z = 0, r = 0, mu = 0, u = 0, rx = 0, hg = 0, act = 0, y = 0, pm = 0, pl = 0, pa = 0, total = 0;
+  size_t z = 0, u = 0, hg = 0, act = 0, y = 0, pm = 0, pl = 0, pa = 0, total = 0;
   int tiles = 0;
 };
 
@@ -440,11 +440,8 @@ DecLayout dec_layout(const ee_exit &e, int64_t n) {
     return o;
   };
   L.z = take(N * h * es);
-  L.r = take(N * 4);
-  L.mu = take(N * 4);
   if (e.kind == EE_EXIT_MLP) {
     L.u = take(N * h * es);
-    L.rx = take(N * 4);
     L.hg = take(N * I * es);
     L.act = take(N * I * es);
     L.y = take(N * h * 4);
@@ -472,26 +469,20 @@ ee_status run_decide(const ee_exit &e, const void *x, int64_t n64, float thresho
   const int I = static_cast<int>(e.intermediate);
   const void *z = x;
   if (e.kind == EE_EXIT_MLP) {
-    EE_LAUNCH("decode mlp pre-norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.rx), s));
-    EE_LAUNCH("decode mlp pre-norm apply", s,
-              ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.rx), e.gamma_mlp, n, n, h, at(ws, L.u), nullptr,
-                                    nullptr, s));
+    EE_LAUNCH("decode mlp pre-norm", s,
+              ee::launch_row_norm(f32, f32, x, n, h, e.rms_eps, e.gamma_mlp, nullptr, false, at(ws, L.u), s));
     EE_LAUNCH("decode gate projection", s, ee::decode_store(f32, e.w_gate, I, at(ws, L.u), n, h, at(ws, L.hg), s));
     EE_LAUNCH("decode up projection + swiglu", s,
               ee::decode_swiglu(f32, e.w_up, I, at(ws, L.u), n, h, at(ws, L.hg), at(ws, L.act), s));
     EE_LAUNCH("decode down projection + residual", s,
               ee::decode_residual(f32, e.w_down, h, at(ws, L.act), n, I, x, atf(ws, L.y), s));
-    EE_LAUNCH("decode exit norm rms", s, ee::launch_row_rms(true, atf(ws, L.y), h, n, h, e.rms_eps, atf(ws, L.r), s));
-    EE_LAUNCH("decode exit norm apply", s,
-              ee::launch_norm_apply(true, f32, atf(ws, L.y), h, atf(ws, L.r), e.gamma, n, n, h, at(ws, L.z), nullptr,
-                                    nullptr, s));
+    EE_LAUNCH("decode exit norm", s,
+              ee::launch_row_norm(true, f32, atf(ws, L.y), n, h, e.rms_eps, e.gamma, nullptr, false, at(ws, L.z), s));
     z = at(ws, L.z);
   } else if (e.kind == EE_EXIT_NORM) {
-    float *mu = e.norm == EE_NORM_LAYER ? atf(ws, L.mu) : nullptr;
-    EE_LAUNCH("decode exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s, mu));
-    EE_LAUNCH("decode exit norm apply", s,
-              ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.r), e.gamma, n, n, h, at(ws, L.z), nullptr, nullptr, s, mu,
-                                    e.beta));
+    EE_LAUNCH("decode exit norm", s,
+              ee::launch_row_norm(f32, f32, x, n, h, e.rms_eps, e.gamma, e.beta, e.norm == EE_NORM_LAYER, at(ws, L.z),
+                                  s));
     z = at(ws, L.z);
   }
   int32_t *pa = reinterpret_cast<int32_t *>(at(ws, L.pa));

@@ -156,6 +156,57 @@ __global__ __launch_bounds__(256) void row_rms_split_kernel(float *x, int n, int
   if (lane == 0) r[row] = 1.0f / sqrtf(s / static_cast<float>(h) + eps);
 }
 
+// Statistics and application of the exit norm in one launch, one block per
+// row, for the few rows of a decode call: z = (x - mu) r * gain (+ bias),
+// mu = 0 unless `centre` (LayerNorm), r from the centred second moment.  The
+// row is read again for each pass (from L1/L2).  h a multiple of 4.
+template <typename Tin, typename T>
+__global__ __launch_bounds__(256) void row_norm_kernel(const Tin *x, int h, float eps, const T *gain, const T *bias,
+                                                       int centre, T *z) {
+  __shared__ float red[4];
+  const int tid = threadIdx.x;
+  const Tin *xr = x + static_cast<int64_t>(blockIdx.x) * h;
+  auto block_sum = [&](float v) {
+    v = warp_sum(v);
+    if ((tid & 63) == 0) red[tid >> 6] = v;
+    __syncthreads();
+    const float t = (red[0] + red[1]) + (red[2] + red[3]);
+    __syncthreads();
+    return t;
+  };
+  float mean = 0.0f;
+  if (centre) {
+    float t = 0.0f;
+    for (int j = tid * 4; j < h; j += 1024) {
+      float v[4];
+      load_f32<4>(xr + j, v);
+      t += (v[0] + v[1]) + (v[2] + v[3]);
+    }
+    mean = block_sum(t) / static_cast<float>(h);
+  }
+  float s = 0.0f;
+  for (int j = tid * 4; j < h; j += 1024) {
+    float v[4];
+    load_f32<4>(xr + j, v);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float c = v[e] - mean;
+      s += c * c;
+    }
+  }
+  const float r = 1.0f / sqrtf(block_sum(s) / static_cast<float>(h) + eps);
+  T *zr = z + static_cast<int64_t>(blockIdx.x) * h;
+  for (int j = tid * 4; j < h; j += 1024) {
+    float v[4], g[4], b[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    load_f32<4>(xr + j, v);
+    load_f32<4>(gain + j, g);
+    if (bias != nullptr) load_f32<4>(bias + j, b);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = (v[e] - mean) * r * g[e] + b[e];
+    store4(zr + j, f32x4_t{v[0], v[1], v[2], v[3]});
+  }
+}
+
 // 64 tokens x 64 features per block.  Row-major outputs are written
 // directly; the token-contiguous copy of x_hat goes through an LDS
 // transpose so that both sides are coalesced.
@@ -537,6 +588,24 @@ hipError_t launch_row_rms_split(float *x, int n, int h, float eps, float *r, Dow
     default:
       return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_row_norm(bool x_f32, bool f32, const void *x, int n, int h, float eps, const void *gain,
+                           const void *bias, bool centre, void *z, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  if (h % 4 != 0 || gain == nullptr) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(n));
+  const int c = centre ? 1 : 0;
+  EE_DISPATCH(f32, {
+    const T *g = static_cast<const T *>(gain), *b = static_cast<const T *>(bias);
+    if (x_f32)
+      hipLaunchKernelGGL((row_norm_kernel<float, T>), grid, dim3(256), 0, stream, static_cast<const float *>(x), h, eps,
+                         g, b, c, static_cast<T *>(z));
+    else
+      hipLaunchKernelGGL((row_norm_kernel<bf16_t, T>), grid, dim3(256), 0, stream, static_cast<const bf16_t *>(x), h,
+                         eps, g, b, c, static_cast<T *>(z));
+  });
   return hipGetLastError();
 }
 

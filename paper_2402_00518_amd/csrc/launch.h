@@ -43,6 +43,12 @@ hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, c
                              void *x_hat_t, hipStream_t stream, const float *mu = nullptr,
                              const void *bias = nullptr);
 
+// The exit norm of a few rows in one launch (decode): z[n][h] = (x - mu) r *
+// gain (+ bias), with mu the row mean when `centre` (LayerNorm), else 0, and
+// r = (mean (x - mu)^2 + eps)^(-1/2).  x is fp32 when x_f32, z is `f32`.
+hipError_t launch_row_norm(bool x_f32, bool f32, const void *x, int n, int h, float eps, const void *gain,
+                           const void *bias, bool centre, void *z, hipStream_t stream);
+
 // Combine the per-tile softmax partials of each token into LSE, the row NLL
 // and the loss weight s_n.  Also flags targets outside [0, V).
 struct CeReduceArgs {
