@@ -116,6 +116,7 @@ CASES = [
     ("norm_wide_vocab", W.EXIT_NORM, 20, 128, 12300, 0, "bf16"),
     ("norm_wide_vocab_f32", W.EXIT_NORM, 12, 64, 12320, 0, "f32"),
     ("mlp_wide_inter", W.EXIT_MLP, 40, 128, 500, 12352, "bf16"),
+    ("norm_max_vocab", W.EXIT_NORM, 3, 64, 1 << 20, 0, "bf16"),
 ]
 
 

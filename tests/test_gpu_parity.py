@@ -122,6 +122,10 @@ SMALL_CASES = [
     # partial sums over a ragged I (mlp_multi_tile: all outputs as two)
     ("mlp_split_tokens", W.EXIT_MLP, 2200, 8192, 300, 1024, "bf16", False),
     ("mlp_split_features", W.EXIT_MLP, 3000, 5440, 300, 1088, "bf16", False),
+    # the most tokens and the largest vocabulary the ABI accepts (2^20 each):
+    # a dW_out product with K = 2^20 in one tile, and 16384 softmax slices
+    ("norm_max_tokens", W.EXIT_NORM, 1 << 20, 64, 40, 0, "bf16", False),
+    ("norm_max_vocab", W.EXIT_NORM, 64, 64, 1 << 20, 0, "bf16", False),
 ]
 
 
