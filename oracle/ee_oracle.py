@@ -35,6 +35,14 @@ Readings where the paper is silent (each also listed in the design notes):
      eps inside the root), z = s_hat * gamma + beta with an optional bias;
      an exit uses one normalisation type for all its norms.
 
+Pins (tests/test_oracle.py): a hand-worked golden example, closed forms at
+W_out = 0, central finite differences, torch autograd in fp64, pure-Python
+brute force, invariances and reordering identities.  The MLP exit's
+arithmetic is pinned the same way, and with W_d = 0 it reduces to the Norm
+exit; but Fig. 2 itself is not in the paper's text, so that R4 is the
+paper's module (rather than another residual pre-norm MLP) is parity
+unpinned.
+
 Every array here is float64; inputs are decoded exactly from their storage
 format before use.  Backward uses the plain chain rule (dZ = G W_out etc.),
 not the reorderings the GPU path uses.
