@@ -302,8 +302,10 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   const int n = static_cast<int>(n64), h = static_cast<int>(e.hidden), V = static_cast<int>(e.vocab);
   const int I = static_cast<int>(e.intermediate), ldn = static_cast<int>(L.ldn);
   const void *zsrc = x;
+  // The first exit of a call clears the device error record in its first kernel.
+  int *clear = first ? reinterpret_cast<int *>(at(ws, kFlagOff)) : nullptr;
   if (e.kind == EE_EXIT_MLP) {
-    EE_LAUNCH("mlp pre-norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.rx), s));
+    EE_LAUNCH("mlp pre-norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.rx), s, nullptr, clear));
     EE_LAUNCH("mlp pre-norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.rx), e.gamma_mlp, n, ldn, h, at(ws, L.u),
                                  at(ws, L.uhat), nullptr, s));
     EE_LAUNCH("gate projection", s, ee::gemm_gate(f32, at(ws, L.u), e.w_gate, n, I, h, at(ws, L.hg), s));
@@ -315,12 +317,13 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
     zsrc = at(ws, L.z);
   } else if (e.kind == EE_EXIT_NORM) {
     float *mu = e.norm == EE_NORM_LAYER ? atf(ws, L.mu) : nullptr;
-    EE_LAUNCH("exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s, mu));
+    EE_LAUNCH("exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s, mu, clear));
     EE_LAUNCH("exit norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.r), e.gamma, n, ldn, h, at(ws, L.z), nullptr,
                                  at(ws, L.zht), s, mu, e.beta));
     zsrc = at(ws, L.z);
   } else {
-    EE_LAUNCH("hidden-state transpose", s, ee::launch_norm_apply(f32, f32, x, h, nullptr, nullptr, n, ldn, h, nullptr, nullptr, at(ws, L.zht), s));
+    EE_LAUNCH("hidden-state transpose", s, ee::launch_norm_apply(f32, f32, x, h, nullptr, nullptr, n, ldn, h, nullptr, nullptr, at(ws, L.zht), s,
+                                                                 nullptr, nullptr, clear));
   }
   EE_LAUNCH("logits + softmax partials", s, ee::gemm_logits(f32, e.w_out, zsrc, V, n, h, at(ws, L.P), ldn, atf(ws, L.pm), atf(ws, L.pl),
                          atf(ws, L.tgt), targets, s));
@@ -555,7 +558,6 @@ ee_status ee_head_forward_loss(const ee_exit *e, const void *hidden, const int32
   EE_TRY(check_aliasing(1, e, hs, targets, token_w, n_tokens, nullptr, loss, 4, row_loss,
                         static_cast<size_t>(n_tokens) * 4, ws, ws_bytes));
   hipStream_t s = static_cast<hipStream_t>(stream);
-  EE_HIP(ee::launch_clear_flag(reinterpret_cast<int *>(at(ws, kFlagOff)), s), "clear error flag");
   return run_forward(*e, hidden, targets, token_w, n_tokens, exit_weight, flags, ws, loss, row_loss, nullptr, 1, s);
 }
 
@@ -603,7 +605,6 @@ ee_status ee_multi_exit_step(int n_exits, const ee_exit *exits, const void *cons
   EE_TRY(check_aliasing(n_exits, exits, hidden, targets, token_w, n_tokens, grads, loss_total, 4, loss_per_exit,
                         static_cast<size_t>(n_exits) * 4, ws, ws_bytes));
   hipStream_t s = static_cast<hipStream_t>(stream);
-  EE_HIP(ee::launch_clear_flag(reinterpret_cast<int *>(at(ws, kFlagOff)), s), "clear error flag");
   for (int i = 0; i < n_exits; ++i) {
     float *loss = loss_per_exit != nullptr ? loss_per_exit + i : atf(ws, kLossSlotOff);
     EE_TRY(run_forward(exits[i], hidden[i], targets, token_w, n_tokens, exit_weights[i], flags, ws, loss, nullptr,

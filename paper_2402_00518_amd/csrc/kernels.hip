@@ -77,14 +77,16 @@ template <int N> __device__ __forceinline__ void store_f32(bf16_t *p, const floa
 // pass over the row (no cancellation from subtracting squared means).
 template <typename Tin>
 __global__ __launch_bounds__(256) void row_rms_kernel(const Tin *x, int64_t ldx, int n, int h, float eps,
-                                                      float *r, float *mu) {
+                                                      float *r, float *mu, int *clear) {
   constexpr int V = 16 / sizeof(Tin);
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (clear != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *clear = 0;  // a step's first kernel
   if (row >= n) return;
   const Tin *xr = x + static_cast<int64_t>(row) * ldx;
   float mean = 0.0f;
   if (mu != nullptr) {
     float t = 0.0f;
+#pragma unroll 4
     for (int j = lane * V; j < h; j += kWave * V) {
       float v[V];
       load_f32<V>(xr + j, v);
@@ -94,6 +96,7 @@ __global__ __launch_bounds__(256) void row_rms_kernel(const Tin *x, int64_t ldx,
     mean = warp_sum(t) / static_cast<float>(h);
   }
   float s = 0.0f;
+#pragma unroll 4
   for (int j = lane * V; j < h; j += kWave * V) {
     float v[V];
     load_f32<V>(xr + j, v);
@@ -213,8 +216,9 @@ __global__ __launch_bounds__(256) void row_norm_kernel(const Tin *x, int h, floa
 template <typename Tin, typename T>
 __global__ __launch_bounds__(256) void norm_apply_kernel(const Tin *x, int64_t ldx, const float *r,
                                                          const float *mu, const T *gain, const T *bias, int n,
-                                                         int ldn, int h, T *z, T *x_hat, T *x_hat_t) {
+                                                         int ldn, int h, T *z, T *x_hat, T *x_hat_t, int *clear) {
   __shared__ float tile[64][65];
+  if (clear != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *clear = 0;  // a step's first kernel
   const int n0 = blockIdx.x * 64, j0 = blockIdx.y * 64;
   const int tid = threadIdx.x;
   const int tr = tid >> 2, tc = (tid & 3) * 16;
@@ -544,7 +548,6 @@ __global__ __launch_bounds__(256) void gain_reduce_kernel(const float *pa, int t
   out[j] = accumulate ? out[j] + total : total;
 }
 
-__global__ void clear_flag_kernel(int *flag) { *flag = 0; }
 
 // -------------------------------------------------------------- launchers
 #define EE_DISPATCH(f32, ...)            \
@@ -559,14 +562,14 @@ __global__ void clear_flag_kernel(int *flag) { *flag = 0; }
   } while (0)
 
 hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps, float *r,
-                          hipStream_t stream, float *mu) {
+                          hipStream_t stream, float *mu, int *clear) {
   const dim3 grid(cdiv(n, 4));
   if (x_f32)
     hipLaunchKernelGGL(row_rms_kernel<float>, grid, dim3(256), 0, stream, static_cast<const float *>(x), ldx,
-                       n, h, eps, r, mu);
+                       n, h, eps, r, mu, clear);
   else
     hipLaunchKernelGGL(row_rms_kernel<bf16_t>, grid, dim3(256), 0, stream, static_cast<const bf16_t *>(x),
-                       ldx, n, h, eps, r, mu);
+                       ldx, n, h, eps, r, mu, clear);
   return hipGetLastError();
 }
 
@@ -611,19 +614,19 @@ hipError_t launch_row_norm(bool x_f32, bool f32, const void *x, int n, int h, fl
 
 hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, const float *r,
                              const void *gain, int n, int ldn, int h, void *z, void *x_hat, void *x_hat_t,
-                             hipStream_t stream, const float *mu, const void *bias) {
+                             hipStream_t stream, const float *mu, const void *bias, int *clear) {
   const dim3 grid(cdiv(ldn, 64), h / 64);
   EE_DISPATCH(f32, {
     if (x_f32)
       hipLaunchKernelGGL((norm_apply_kernel<float, T>), grid, dim3(256), 0, stream,
                          static_cast<const float *>(x), ldx, r, mu, static_cast<const T *>(gain),
                          static_cast<const T *>(bias), n, ldn, h, static_cast<T *>(z), static_cast<T *>(x_hat),
-                         static_cast<T *>(x_hat_t));
+                         static_cast<T *>(x_hat_t), clear);
     else
       hipLaunchKernelGGL((norm_apply_kernel<bf16_t, T>), grid, dim3(256), 0, stream,
                          static_cast<const bf16_t *>(x), ldx, r, mu, static_cast<const T *>(gain),
                          static_cast<const T *>(bias), n, ldn, h, static_cast<T *>(z), static_cast<T *>(x_hat),
-                         static_cast<T *>(x_hat_t));
+                         static_cast<T *>(x_hat_t), clear);
   });
   return hipGetLastError();
 }
@@ -677,10 +680,6 @@ hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const floa
   return hipGetLastError();
 }
 
-hipError_t launch_clear_flag(int *flag, hipStream_t stream) {
-  hipLaunchKernelGGL(clear_flag_kernel, dim3(1), dim3(1), 0, stream, flag);
-  return hipGetLastError();
-}
 
 // ------------------------------------------------------------------ GEMMs
 // bf16 GEMMs whose operands are both K-major take the 256 x 256 tile; the

@@ -26,8 +26,10 @@ int gemm_part_cols(bool f32);
 // Row statistics of the exit norm.  RMSNorm (mu == NULL): r[n] =
 // (mean_j x[n][j]^2 + eps)^(-1/2).  LayerNorm: mu[n] = mean_j x[n][j] and
 // r[n] = (mean_j (x[n][j] - mu[n])^2 + eps)^(-1/2).
+// clear (optional): the device error flag, set to 0 by the launch (the
+// first kernel of a step clears it instead of a launch of its own).
 hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps,
-                          float *r, hipStream_t stream, float *mu = nullptr);
+                          float *r, hipStream_t stream, float *mu = nullptr, int *clear = nullptr);
 // RMSNorm statistics of the fp32 rows the split down projection leaves
 // (see gemm_down_residual): the split outputs are first replaced by the sum
 // of their slices, in slice order.
@@ -37,11 +39,11 @@ hipError_t launch_row_rms_split(float *x, int n, int h, float eps, float *r, Dow
 // (mu == NULL: no centring; r == NULL: no scale), z = x_hat * gain + bias
 // (bias may be NULL).  Writes any of z [n][h], x_hat [n][h] (row-major) and
 // x_hat^T [h][ldn] (token-contiguous, columns n..ldn-1 zero).  Output
-// element type = `f32`.
+// element type = `f32`.  clear: as for launch_row_rms.
 hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, const float *r,
                              const void *gain, int n, int ldn, int h, void *z, void *x_hat,
                              void *x_hat_t, hipStream_t stream, const float *mu = nullptr,
-                             const void *bias = nullptr);
+                             const void *bias = nullptr, int *clear = nullptr);
 
 // The exit norm of a few rows in one launch (decode): z[n][h] = (x - mu) r *
 // gain (+ bias), with mu the row mean when `centre` (LayerNorm), else 0, and
@@ -90,7 +92,6 @@ hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *par
 hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const float *r, const void *gain,
                            int n, int h, void *dy, hipStream_t stream, int splits = 1, int64_t zstride = 0);
 
-hipError_t launch_clear_flag(int *flag, hipStream_t stream);
 
 // ------------------------------------------------------------------ GEMMs
 // Logits^T = W_out Z^T with the softmax-partials epilogue.
