@@ -533,6 +533,42 @@ struct EpiResidualTr {
   }
 };
 
+// Backward of the SwiGLU product, untransposed (rows of C = dA = dY W_down
+// are tokens, columns features i; lanes 0-31 of each access cover 32
+// consecutive features of one token):
+//   dH_g = dA * H_u * silu'(H_g),   dH_u = dA * silu(H_g).
+template <typename T>
+struct EpiSwiGLUBwd {
+  struct Params {
+    const T *Hg;   // [N][ld]
+    const T *Hu;
+    T *dHg;
+    T *dHu;
+    int64_t ld;
+  };
+  struct H2 {
+    T g, u;
+  };
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    for_each_acc_loaded<Cfg>(
+        acc, t, t.M, t.N,
+        [&](int row, int col) EE_ALWAYS_INLINE {
+          const int64_t o = static_cast<int64_t>(row) * p.ld + col;
+          return H2{p.Hg[o], p.Hu[o]};
+        },
+        [&](int row, int col, int, float da, H2 h) EE_ALWAYS_INLINE {
+          if (row < t.M && col < t.N) {
+            const int64_t o = static_cast<int64_t>(row) * p.ld + col;
+            float sv, sg;
+            silu_and_grad(to_f32(h.g), sv, sg);
+            p.dHg[o] = from_f32<T>(da * to_f32(h.u) * sg);
+            p.dHu[o] = from_f32<T>(da * sv);
+          }
+        });
+  }
+};
+
 // Backward of the SwiGLU product from dA[n][i] = C[i][n] (C = W_down^T dY^T):
 //   dH_g = dA * H_u * silu'(H_g),   dH_u = dA * silu(H_g).
 template <typename T>

@@ -884,11 +884,11 @@ hipError_t gemm_da_swiglu_dw_down(bool f32, const void *dy, const void *w_down, 
                                  const void *hg, const void *hu, void *dhg, void *dhu, const void *act, float *dwd,
                                  int accumulate, hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiSwiGLUBwdTr<T>::Params e1{static_cast<const T *>(hg), static_cast<const T *>(hu),
-                                          static_cast<T *>(dhg), static_cast<T *>(dhu), inter};
+    typename EpiSwiGLUBwd<T>::Params e1{static_cast<const T *>(hg), static_cast<const T *>(hu),
+                                        static_cast<T *>(dhg), static_cast<T *>(dhu), inter};
     typename EpiStoreF32<T>::Params e2{dwd, inter, h, accumulate};
-    return run_gemm_pair<T, false, true, EpiSwiGLUBwdTr<T>, false, false, EpiStoreF32<T>>(
-        Operand{w_down, inter}, Operand{dy, h}, GemmShape{inter, n, h}, e1, Operand{dy, h}, Operand{act, inter},
+    return run_gemm_pair<T, true, false, EpiSwiGLUBwd<T>, false, false, EpiStoreF32<T>>(
+        Operand{dy, h}, Operand{w_down, inter}, GemmShape{n, inter, h}, e1, Operand{dy, h}, Operand{act, inter},
         GemmShape{h, inter, n}, e2, stream);
   });
   return hipSuccess;

@@ -38,7 +38,7 @@ LABEL_KERNELS = {
     "gate projection": "ee::EpiStoreTr<",
     "up projection + swiglu": "ee::EpiSwiGLU<",
     "down projection + residual": "ee::EpiResidualTr<",
-    "dA + swiglu backward, down gradient": "ee::EpiSwiGLUBwdTr<",
+    "dA + swiglu backward, down gradient": "ee::EpiSwiGLUBwd<",
     "logit seed": "seed_kernel",
     "cross-entropy reduce": "ce_reduce_kernel",
 }
