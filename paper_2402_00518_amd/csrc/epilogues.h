@@ -44,48 +44,6 @@ __device__ __forceinline__ void for_each_acc_loaded(f32x16_t (&acc)[Cfg::MB][Cfg
   });
 }
 
-// Row-vector form, for outputs stored transposed (C[m][n] at ptr[n*ld + m]):
-// a lane's accumulator rows 4q..4q+3 of a block are consecutive, so they
-// are one 8-byte (bf16) or 16-byte (fp32) access there.  f(row0, col, j,
-// vals, loaded) runs for every such group of 32-row block i once the
-// load(row0_c, col_c) of the whole block are in, and the loads of block i + 1
-// are issued before block i is processed (row0 and col clamped into the
-// problem; the row count must be a multiple of 4).  A 128-byte bf16 line of
-// the output spans two blocks; with the next block's loads already in flight
-// its two halves reach L2 sooner after each other (under the main loop's
-// operand streaming a half-written line can be evicted within microseconds
-// and is then written twice).
-template <class Cfg, class L, class F>
-__device__ __forceinline__ void for_each_acc4_loaded(f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t,
-                                                     L &&load, F &&f) {
-  using V = decltype(load(0, 0));
-  V pre[2][4][Cfg::NB];
-  auto issue = [&](auto blk) EE_ALWAYS_INLINE {
-    constexpr int I = decltype(blk)::value;
-    if constexpr (I < Cfg::MB) {
-      static_for<4>([&](auto q) EE_ALWAYS_INLINE {
-        const int row0 = min(t.row(I, 4 * q), t.M - 4);
-        static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE {
-          pre[I % 2][decltype(q)::value][j] = load(row0, min(t.col(j), t.N - 1));
-        });
-      });
-    }
-  };
-  issue(std::integral_constant<int, 0>{});
-  static_for<Cfg::MB>([&](auto i) EE_ALWAYS_INLINE {
-    constexpr int I = decltype(i)::value;
-    issue(std::integral_constant<int, I + 1>{});
-    static_for<4>([&](auto q) EE_ALWAYS_INLINE {
-      constexpr int v0 = 4 * decltype(q)::value;
-      const int row0 = t.row(I, v0);
-      static_for<Cfg::NB>([&](auto j) EE_ALWAYS_INLINE {
-        const f32x4_t c = {acc[I][j][v0], acc[I][j][v0 + 1], acc[I][j][v0 + 2], acc[I][j][v0 + 3]};
-        f(row0, t.col(j), static_cast<int>(j), c, pre[I % 2][decltype(q)::value][j]);
-      });
-    });
-  });
-}
-
 // Four consecutive elements as fp32, and back.
 __device__ __forceinline__ f32x4_t load4(const float *p) { return *reinterpret_cast<const f32x4_t *>(p); }
 __device__ __forceinline__ f32x4_t load4(const bf16_t *p) {
@@ -454,26 +412,51 @@ struct EpiStoreF32 {
   }
 };
 
-// The SwiGLU MLP's GEMMs run transposed: rows of C are features (I or h)
-// and columns are tokens, while every activation is stored token-major
-// ([N][I] or [N][h]), so each lane's four consecutive rows are one vector
-// access.  Feature counts are multiples of 64, so a group of four rows is
-// either wholly inside the problem or wholly outside.
-
-// Gate projection: H_g[n][i] = C[i][n], stored in the element type.
+// Plain store in the element type, untransposed: C[row][col] (gate
+// projection with tokens as rows: H_g[n][i]).  Lanes 0-31 of each store
+// cover 32 consecutive columns of one row.
 template <typename T>
-struct EpiStoreTr {
+struct EpiStore {
   struct Params {
-    T *C;          // [N][ldc]
+    T *C;          // [M][ldc]
     int64_t ldc;
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc4_loaded<Cfg>(
-        acc, t, [&](int, int) EE_ALWAYS_INLINE { return 0; },
-        [&](int row0, int col, int, f32x4_t c, int) EE_ALWAYS_INLINE {
-          if (row0 < t.M && col < t.N) store4(p.C + static_cast<int64_t>(col) * p.ldc + row0, c);
-        });
+    for_each_acc<Cfg>(acc, t, [&](int row, int col, int, float a) EE_ALWAYS_INLINE {
+      if (row < t.M && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = from_f32<T>(a);
+    });
+  }
+};
+
+// Down projection with the residual, untransposed (rows of C are tokens,
+// columns features): Y[n][j] = X[n][j] + C[n][j]  (fp32 out; lanes 0-31 of a
+// store write one 128-byte line).  With split K, slice z of the product goes
+// to Y + z * zstride and only slice 0 adds X (the slices are partial sums
+// the exit-norm statistics add).
+template <typename T>
+struct EpiResidual {
+  struct Params {
+    float *Y;       // [N][ld]
+    const T *X;     // [N][ld]
+    int64_t ld;
+    int64_t zstride;
+  };
+  template <class Cfg>
+  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
+    float *Y = p.Y + t.kz * p.zstride;
+    if (t.kz == 0) {
+      for_each_acc_loaded<Cfg>(
+          acc, t, t.M, t.N,
+          [&](int row, int col) EE_ALWAYS_INLINE { return p.X[static_cast<int64_t>(row) * p.ld + col]; },
+          [&](int row, int col, int, float a, T x) EE_ALWAYS_INLINE {
+            if (row < t.M && col < t.N) Y[static_cast<int64_t>(row) * p.ld + col] = a + to_f32(x);
+          });
+    } else {
+      for_each_acc<Cfg>(acc, t, [&](int row, int col, int, float a) EE_ALWAYS_INLINE {
+        if (row < t.M && col < t.N) Y[static_cast<int64_t>(row) * p.ld + col] = a;
+      });
+    }
   }
 };
 
@@ -500,36 +483,6 @@ struct EpiSwiGLU {
             p.A[o] = from_f32<T>(silu_f(hg) * hu);
           }
         });
-  }
-};
-
-// Down projection with the residual: Y[n][j] = X[n][j] + C[j][n]  (fp32 out).
-// With split K, slice z of the product goes to Y + z * zstride and only
-// slice 0 adds X (the slices are partial sums the exit-norm statistics add).
-template <typename T>
-struct EpiResidualTr {
-  struct Params {
-    float *Y;       // [N][ld]
-    const T *X;     // [N][ld]
-    int64_t ld;
-    int64_t zstride;
-  };
-  template <class Cfg>
-  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    float *Y = p.Y + t.kz * p.zstride;
-    if (t.kz == 0) {
-      for_each_acc4_loaded<Cfg>(
-          acc, t, [&](int row0, int col) EE_ALWAYS_INLINE { return raw4(p.X + static_cast<int64_t>(col) * p.ld + row0); },
-          [&](int row0, int col, int, f32x4_t c, Raw4<T> x) EE_ALWAYS_INLINE {
-            if (row0 < t.M && col < t.N) store4(Y + static_cast<int64_t>(col) * p.ld + row0, c + cvt4(x));
-          });
-    } else {
-      for_each_acc4_loaded<Cfg>(
-          acc, t, [&](int, int) EE_ALWAYS_INLINE { return 0; },
-          [&](int row0, int col, int, f32x4_t c, int) EE_ALWAYS_INLINE {
-            if (row0 < t.M && col < t.N) store4(Y + static_cast<int64_t>(col) * p.ld + row0, c);
-          });
-    }
   }
 };
 
@@ -564,47 +517,6 @@ struct EpiSwiGLUBwd {
             silu_and_grad(to_f32(h.g), sv, sg);
             p.dHg[o] = from_f32<T>(da * to_f32(h.u) * sg);
             p.dHu[o] = from_f32<T>(da * sv);
-          }
-        });
-  }
-};
-
-// Backward of the SwiGLU product from dA[n][i] = C[i][n] (C = W_down^T dY^T):
-//   dH_g = dA * H_u * silu'(H_g),   dH_u = dA * silu(H_g).
-template <typename T>
-struct EpiSwiGLUBwdTr {
-  struct Params {
-    const T *Hg;
-    const T *Hu;
-    T *dHg;
-    T *dHu;
-    int64_t ld;
-  };
-  struct R2 {
-    Raw4<T> a, b;
-  };
-  template <class Cfg>
-  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc4_loaded<Cfg>(
-        acc, t,
-        [&](int row0, int col) EE_ALWAYS_INLINE {
-          const int64_t o = static_cast<int64_t>(col) * p.ld + row0;
-          return R2{raw4(p.Hg + o), raw4(p.Hu + o)};
-        },
-        [&](int row0, int col, int, f32x4_t da, R2 h) EE_ALWAYS_INLINE {
-          if (row0 < t.M && col < t.N) {
-            const int64_t o = static_cast<int64_t>(col) * p.ld + row0;
-            const f32x4_t hg = cvt4(h.a), hu = cvt4(h.b);
-            f32x4_t dg, du;
-            static_for<4>([&](auto e) EE_ALWAYS_INLINE {
-              constexpr int E = decltype(e)::value;
-              float sv, sg;
-              silu_and_grad(hg[E], sv, sg);
-              dg[E] = da[E] * hu[E] * sg;
-              du[E] = da[E] * sv;
-            });
-            store4(p.dHg + o, dg);
-            store4(p.dHu + o, du);
           }
         });
   }

@@ -742,9 +742,9 @@ hipError_t gemm_weight_grad_mn_pair(bool f32, const void *g1, const void *g2, co
 hipError_t gemm_gate(bool f32, const void *u, const void *w_gate, int n, int inter, int h, void *hg,
                      hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiStoreTr<T>::Params ep{static_cast<T *>(hg), inter};
-    return run_gemm<T, true, true, EpiStoreTr<T>>(Operand{w_gate, h}, Operand{u, h}, GemmShape{inter, n, h},
-                                                     ep, stream);
+    typename EpiStore<T>::Params ep{static_cast<T *>(hg), inter};
+    return run_gemm<T, true, true, EpiStore<T>>(Operand{u, h}, Operand{w_gate, h}, GemmShape{n, inter, h}, ep,
+                                                   stream);
   });
   return hipSuccess;
 }
@@ -764,23 +764,24 @@ hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, con
                               int inter, float *y, hipStream_t stream, DownSplit sp) {
   EE_DISPATCH(f32, {
     const T *xt = static_cast<const T *>(x), *at = static_cast<const T *>(act), *wd = static_cast<const T *>(w_down);
-    // Split region: tokens [t0, n) x features [f0, h).  The rest takes all of
-    // K: tokens [0, t0) (f0 == 0) or features [0, f0) (t0 == 0).
+    // Tiles: tokens as rows, features as columns.  Split region: tokens
+    // [t0, n) x features [f0, h).  The rest takes all of K: tokens [0, t0)
+    // (f0 == 0) or features [0, f0) (t0 == 0).
     const bool split = sp.splits > 1;
     const int t0 = split ? sp.tok0 : n, f0 = split ? sp.feat0 : 0;
     if (t0 < 0 || t0 > n || f0 < 0 || f0 > h || (t0 > 0 && f0 > 0)) return hipErrorInvalidValue;
-    const int m1 = t0 > 0 ? h : f0, n1 = t0 > 0 ? t0 : n;
+    const int m1 = t0 > 0 ? t0 : n, n1 = t0 > 0 ? h : f0;
     const int64_t o = static_cast<int64_t>(t0) * h + f0;
-    typename EpiResidualTr<T>::Params e1{y, xt, h, 0};
-    typename EpiResidualTr<T>::Params e2{y + o, xt + o, h, static_cast<int64_t>(n) * h};
-    GemmShape s2{h - f0, n - t0, inter};
+    typename EpiResidual<T>::Params e1{y, xt, h, 0};
+    typename EpiResidual<T>::Params e2{y + o, xt + o, h, static_cast<int64_t>(n) * h};
+    GemmShape s2{n - t0, h - f0, inter};
     if (split) {
       s2.kchunk = split_kchunk(inter, sp.splits);
       if (cdiv(inter, s2.kchunk) != sp.splits) return hipErrorInvalidValue;  // Y holds sp.splits slices
     }
-    return run_gemm_pair<T, true, true, EpiResidualTr<T>, true, true, EpiResidualTr<T>>(
-        Operand{wd, inter}, Operand{at, inter}, GemmShape{m1, n1, inter}, e1,
-        Operand{wd + static_cast<int64_t>(f0) * inter, inter}, Operand{at + static_cast<int64_t>(t0) * inter, inter},
+    return run_gemm_pair<T, true, true, EpiResidual<T>, true, true, EpiResidual<T>>(
+        Operand{at, inter}, Operand{wd, inter}, GemmShape{m1, n1, inter}, e1,
+        Operand{at + static_cast<int64_t>(t0) * inter, inter}, Operand{wd + static_cast<int64_t>(f0) * inter, inter},
         s2, e2, stream);
   });
   return hipSuccess;

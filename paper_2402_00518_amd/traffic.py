@@ -35,9 +35,9 @@ LABEL_KERNELS = {
     "output-matrix gradient": "gemm_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
     "dZ": "gemm_kernel<unsigned short, false, false, ee::EpiStoreF32<",
     "gate and up gradients": "gemm_pair_kernel<unsigned short, false, false, ee::EpiWeightGrad<",
-    "gate projection": "ee::EpiStoreTr<",
+    "gate projection": "ee::EpiStore<",
     "up projection + swiglu": "ee::EpiSwiGLU<",
-    "down projection + residual": "ee::EpiResidualTr<",
+    "down projection + residual": "ee::EpiResidual<",
     "dA + swiglu backward, down gradient": "ee::EpiSwiGLUBwd<",
     "logit seed": "seed_kernel",
     "cross-entropy reduce": "ce_reduce_kernel",
