@@ -47,8 +47,8 @@ struct Layout {
   size_t u = 0, uhat = 0, rx = 0, hg = 0, hu = 0, act = 0, y = 0, dz = 0, dy = 0, dhg = 0, dhu = 0,
          dgpg = 0, dgpu = 0;
   size_t mu = 0, gsp = 0, gsum = 0, dbp = 0;  // LayerNorm mean; bias: G row sums, bias partials
-  int dzs = 1;                                // split-K slices of the dZ product
-  ee::DownSplit ys{0, 0, 1};                  // split-K tail of the down projection
+  ee::SplitTail zs{0, 0, 1};                  // split-K tail of the dZ product
+  ee::SplitTail ys{0, 0, 1};                  // split-K tail of the down projection
   int64_t gchunks = 0;
   size_t total = 0;
 };
@@ -100,10 +100,10 @@ Layout layout(const ee_exit &e, int64_t n) {
     L.hg = take(N * I * es);
     L.hu = take(N * I * es);
     L.act = take(N * I * es);
-    L.ys = ee::down_split(f32, static_cast<int>(n), static_cast<int>(h), static_cast<int>(I));
+    L.ys = ee::split_tail(f32, static_cast<int>(n), static_cast<int>(h), static_cast<int>(I));
     L.y = take(static_cast<size_t>(L.ys.splits) * N * h * 4);
-    L.dzs = ee::dz_splits(f32, static_cast<int>(L.ldn), static_cast<int>(h), static_cast<int>(V));
-    L.dz = take(static_cast<size_t>(L.dzs) * N * h * 4);
+    L.zs = ee::split_tail(f32, static_cast<int>(n), static_cast<int>(h), static_cast<int>(V));
+    L.dz = take(static_cast<size_t>(L.zs.splits) * N * h * 4);
     L.dy = take(N * h * es);
     L.dhg = take(N * I * es);
     L.dhu = take(N * I * es);
@@ -371,9 +371,9 @@ ee_status run_backward(const ee_exit &e, int64_t n64, void *ws, const ee_exit_gr
   if (bias)
     EE_LAUNCH("exit bias gradient", s, ee::launch_gain_reduce(atf(ws, L.dbp), static_cast<int>(L.vtiles), nullptr, 0, h, g.d_beta, acc, s));
   if (e.kind != EE_EXIT_MLP) return EE_OK;
-  EE_LAUNCH("dZ", s, ee::gemm_dz(f32, at(ws, L.P), e.w_out, n, ldn, h, V, atf(ws, L.dz), s, L.dzs));
+  EE_LAUNCH("dZ", s, ee::gemm_dz(f32, at(ws, L.P), e.w_out, n, ldn, h, V, atf(ws, L.dz), s, L.zs));
   EE_LAUNCH("exit norm backward", s, ee::launch_norm_bwd(f32, atf(ws, L.dz), atf(ws, L.y), atf(ws, L.r), e.gamma, n, h, at(ws, L.dy), s,
-                                                         L.dzs, static_cast<int64_t>(n) * h));
+                                                         L.zs));
   EE_LAUNCH("dA + swiglu backward, down gradient", s,
             ee::gemm_da_swiglu_dw_down(f32, at(ws, L.dy), e.w_down, n, I, h, at(ws, L.hg), at(ws, L.hu), at(ws, L.dhg),
                                        at(ws, L.dhu), at(ws, L.act), g.d_w_down, acc, s));

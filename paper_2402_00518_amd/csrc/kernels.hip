@@ -269,11 +269,11 @@ __global__ __launch_bounds__(256) void norm_apply_kernel(const Tin *x, int64_t l
 // RMSNorm backward, one wave per row (see launch.h for the formula).
 constexpr int kNormBwdMaxH = 16 * kWave * 8;  // 8192: at most 16 8-wide chunks per lane
 
-// dZ arrives as `splits` partial sums zstride apart (split-K GEMM), added
-// here in slice order.
-__device__ __forceinline__ void load_dz8(const float *dz, int64_t o, int splits, int64_t zstride, float (&a)[8]) {
+// dZ arrives as partial sums zstride apart (split-K GEMM): ns slices at
+// this position, added here in slice order.
+__device__ __forceinline__ void load_dz8(const float *dz, int64_t o, int ns, int64_t zstride, float (&a)[8]) {
   load_f32<8>(dz + o, a);
-  for (int z = 1; z < splits; ++z) {
+  for (int z = 1; z < ns; ++z) {
     float t[8];
     load_f32<8>(dz + z * zstride + o, t);
 #pragma unroll
@@ -282,8 +282,9 @@ __device__ __forceinline__ void load_dz8(const float *dz, int64_t o, int splits,
 }
 
 template <typename T, int CH>
-__global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int splits, int64_t zstride, const float *y,
-                                                       const float *r, const T *gain, int n, int h, T *dy) {
+__global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int splits, int64_t zstride, int tok0,
+                                                       int feat0, const float *y, const float *r, const T *gain, int n,
+                                                       int h, T *dy) {
   // One wave per row; the row's dZ * gain stays in registers (CH 8-wide
   // chunks per lane, h <= CH * 512) between the projection and the output,
   // so dZ's slices are read once.
@@ -291,6 +292,7 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int spli
   if (row >= n) return;
   const int64_t o = static_cast<int64_t>(row) * h;
   const float rr = r[row];
+  const int f0 = row >= tok0 ? feat0 : h;  // features from f0 on are split
   float dg[CH][8];
   float s = 0.0f;
 #pragma unroll
@@ -298,7 +300,7 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int spli
     const int j = (c * kWave + lane) * 8;
     if (j < h) {
       float g[8], yy[8];
-      load_dz8(dz, o + j, splits, zstride, dg[c]);
+      load_dz8(dz, o + j, j >= f0 ? splits : 1, zstride, dg[c]);
       load_f32<8>(y + o + j, yy);
       load_f32<8>(gain + j, g);
 #pragma unroll
@@ -573,7 +575,7 @@ hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, 
   return hipGetLastError();
 }
 
-hipError_t launch_row_rms_split(float *x, int n, int h, float eps, float *r, DownSplit sp, hipStream_t stream) {
+hipError_t launch_row_rms_split(float *x, int n, int h, float eps, float *r, SplitTail sp, hipStream_t stream) {
   if (sp.splits <= 1) return launch_row_rms(true, x, h, n, h, eps, r, stream);
   if (h % 4 != 0 || sp.tok0 < 0 || sp.tok0 > n || sp.feat0 < 0 || sp.feat0 > h) return hipErrorInvalidValue;
   const dim3 grid(cdiv(n, 4));
@@ -662,20 +664,24 @@ hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *par
 }
 
 hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const float *r, const void *gain, int n,
-                           int h, void *dy, hipStream_t stream, int splits, int64_t zstride) {
+                           int h, void *dy, hipStream_t stream, SplitTail sp) {
   if (h > kNormBwdMaxH) return hipErrorInvalidValue;
+  const int splits = sp.splits > 1 ? sp.splits : 1;
+  const int t0 = splits > 1 ? sp.tok0 : n, f0 = splits > 1 ? sp.feat0 : h;
+  if (t0 < 0 || t0 > n || f0 < 0 || f0 > h) return hipErrorInvalidValue;
+  const int64_t zs = static_cast<int64_t>(n) * h;
   const dim3 grid(cdiv(n, 4));
   EE_DISPATCH(f32, {
     const T *g = static_cast<const T *>(gain);
     T *d = static_cast<T *>(dy);
     if (h <= 2048)
-      hipLaunchKernelGGL((norm_bwd_kernel<T, 4>), grid, dim3(256), 0, stream, dz, splits, zstride, y, r, g, n, h, d);
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 4>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d);
     else if (h <= 4096)
-      hipLaunchKernelGGL((norm_bwd_kernel<T, 8>), grid, dim3(256), 0, stream, dz, splits, zstride, y, r, g, n, h, d);
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 8>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d);
     else if (h <= 6144)
-      hipLaunchKernelGGL((norm_bwd_kernel<T, 12>), grid, dim3(256), 0, stream, dz, splits, zstride, y, r, g, n, h, d);
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 12>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d);
     else
-      hipLaunchKernelGGL((norm_bwd_kernel<T, 16>), grid, dim3(256), 0, stream, dz, splits, zstride, y, r, g, n, h, d);
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 16>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d);
   });
   return hipGetLastError();
 }
@@ -761,7 +767,7 @@ hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int 
 }
 
 hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, const void *x, int n, int h,
-                              int inter, float *y, hipStream_t stream, DownSplit sp) {
+                              int inter, float *y, hipStream_t stream, SplitTail sp) {
   EE_DISPATCH(f32, {
     const T *xt = static_cast<const T *>(x), *at = static_cast<const T *>(act), *wd = static_cast<const T *>(w_down);
     // Tiles: tokens as rows, features as columns.  Split region: tokens
@@ -815,20 +821,26 @@ double launch_span(int64_t full, int64_t parts, int K, int kchunk) {
 
 int split_kchunk(int K, int splits) { return cdiv(cdiv(K, splits), 64) * 64; }
 
-DownSplit down_split(bool f32, int n, int h, int inter) {
-  DownSplit best{n, 0, 1};
+SplitTail split_tail(bool f32, int n, int h, int K) {
+  SplitTail best{n, 0, 1};
   if (f32 || n <= 0) return best;
-  static thread_local int key[3] = {-1, -1, -1};
-  static thread_local DownSplit memo{0, 0, 1};
-  if (key[0] == n && key[1] == h && key[2] == inter) return memo;
+  // the last few shapes asked for (a layout asks for two per call)
+  struct Memo {
+    int n = -1, h = -1, K = -1;
+    SplitTail sp{0, 0, 1};
+  };
+  static thread_local Memo memo[4];
+  static thread_local int next = 0;
+  for (const Memo &m : memo)
+    if (m.n == n && m.h == h && m.K == K) return m.sp;
   const int tm = cdiv(h, CfgBig::BM), tn = cdiv(n, CfgBig::BN);
   const int64_t tiles = static_cast<int64_t>(tm) * tn;
   if (tiles < 4 * kCus) {
     const int64_t rounds = tiles / kCus;
-    double best_span = 0.9 * launch_span(tiles, 0, inter, inter);
+    double best_span = 0.9 * launch_span(tiles, 0, K, K);
     for (int s = 2; s <= 4; s *= 2) {
-      if (inter / s < 4 * 64) break;
-      const int kc = split_kchunk(inter, s), slices = cdiv(inter, kc);
+      if (K / s < 4 * 64) break;
+      const int kc = split_kchunk(K, s), slices = cdiv(K, kc);
       // Split the last c token blocks (dim 0) or feature blocks (dim 1):
       // all of them, or the fewest that leave the whole-K tiles one or two
       // rounds short of the current count.
@@ -839,13 +851,13 @@ DownSplit down_split(bool f32, int n, int h, int inter) {
           if (rounds - r >= 0) cand[r + 1] = static_cast<int>((tiles - (rounds - r) * kCus + across - 1) / across);
         for (int c : cand) {
           if (c < 1 || c > blocks) continue;
-          const DownSplit sp = dim == 0 ? DownSplit{(tn - c) * CfgBig::BN, 0, slices}
-                                        : DownSplit{0, (tm - c) * CfgBig::BM, slices};
+          const SplitTail sp = dim == 0 ? SplitTail{(tn - c) * CfgBig::BN, 0, slices}
+                                        : SplitTail{0, (tm - c) * CfgBig::BM, slices};
           // extra HBM traffic: slices 1.. written and read back, their sum written
           const double outs = static_cast<double>(n - sp.tok0) * (h - sp.feat0);
           const double extra = outs * 4 * (2 * (slices - 1) + 1) / kBytesPerK;
           const double span = launch_span(static_cast<int64_t>(blocks - c) * across,
-                                          static_cast<int64_t>(c) * across * slices, inter, kc) + extra;
+                                          static_cast<int64_t>(c) * across * slices, K, kc) + extra;
           if (span < best_span) {
             best_span = span;
             best = sp;
@@ -854,29 +866,36 @@ DownSplit down_split(bool f32, int n, int h, int inter) {
       }
     }
   }
-  key[0] = n, key[1] = h, key[2] = inter;
-  memo = best;
+  memo[next] = Memo{n, h, K, best};
+  next = (next + 1) % 4;
   return best;
 }
 
-int dz_splits(bool f32, int ldn, int h, int vocab) {
-  // Split K until the product has about four rounds of tiles on the GPU's
-  // 256 CUs (a shape-only rule, so results do not depend on the device):
-  // at most 4 slices, each at least 4 stages deep.
-  if (f32) return 1;
-  const int tiles = cdiv(ldn, CfgBig::BM) * cdiv(h, CfgBig::BN);
-  int s = 1;
-  while (s < 4 && tiles * s < 1024 && vocab / (2 * s) >= 4 * 64) s *= 2;
-  return cdiv(vocab, split_kchunk(vocab, s));
-}
-
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab, float *dz,
-                   hipStream_t stream, int splits) {
+                   hipStream_t stream, SplitTail sp) {
   EE_DISPATCH(f32, {
-    typename EpiStoreF32<T>::Params ep{dz, h, n, 0, static_cast<int64_t>(n) * h};
-    GemmShape sh{ldn, h, vocab};
-    if (splits > 1) sh.kchunk = split_kchunk(vocab, splits);
-    return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{g_t, ldn}, Operand{w_out, h}, sh, ep, stream);
+    const T *gt = static_cast<const T *>(g_t), *wo = static_cast<const T *>(w_out);
+    // Tiles: tokens (padded to ldn; rows past n are not stored) as rows,
+    // features as columns, both operands read MN-major.  Split region:
+    // tokens [t0, n) x features [f0, h); the rest takes all of K: tokens
+    // [0, t0) (f0 == 0) or features [0, f0) (t0 == 0).
+    if (sp.splits <= 1) {
+      typename EpiStoreF32<T>::Params ep{dz, h, n, 0, 0};
+      return run_gemm<T, false, false, EpiStoreF32<T>>(Operand{gt, ldn}, Operand{wo, h}, GemmShape{ldn, h, vocab}, ep,
+                                                        stream);
+    }
+    const int t0 = sp.tok0, f0 = sp.feat0;
+    if (t0 < 0 || t0 > n || t0 % 64 != 0 || f0 < 0 || f0 > h || (t0 > 0 && f0 > 0)) return hipErrorInvalidValue;
+    const int m1 = t0 > 0 ? t0 : ldn, n1 = t0 > 0 ? h : f0;
+    typename EpiStoreF32<T>::Params e1{dz, h, t0 > 0 ? t0 : n, 0, 0};
+    typename EpiStoreF32<T>::Params e2{dz + static_cast<int64_t>(t0) * h + f0, h, n - t0, 0,
+                                       static_cast<int64_t>(n) * h};
+    GemmShape s2{ldn - t0, h - f0, vocab};
+    s2.kchunk = split_kchunk(vocab, sp.splits);
+    if (cdiv(vocab, s2.kchunk) != sp.splits) return hipErrorInvalidValue;  // dZ holds sp.splits slices
+    return run_gemm_pair<T, false, false, EpiStoreF32<T>, false, false, EpiStoreF32<T>>(
+        Operand{gt, ldn}, Operand{wo, h}, GemmShape{m1, n1, vocab}, e1, Operand{gt + t0, ldn}, Operand{wo + f0, h}, s2,
+        e2, stream);
   });
   return hipSuccess;
 }

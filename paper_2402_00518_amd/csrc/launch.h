@@ -10,10 +10,12 @@ namespace ee {
 
 constexpr int kTokenPad = 64;     // padding of the token dimension
 
-// Split-K tail of the MLP exit's down projection (gemm_down_residual): the
-// outputs of tokens >= tok0 and features >= feat0 (one of the two is 0) are
-// computed as `splits` partial sums over slices of K; the rest take all of K.
-struct DownSplit {
+// Split-K tail of the MLP exit's token-by-feature products (the down
+// projection and dZ): the outputs of tokens >= tok0 and features >= feat0
+// (one of the two is 0) are computed as `splits` partial sums over slices of
+// K, slice z at z * n * h floats from slice 0; the rest take all of K.
+// split_tail(f32, n, h, K) picks one for a shape.
+struct SplitTail {
   int tok0;
   int feat0;
   int splits;  // 1: no split
@@ -33,7 +35,7 @@ hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, 
 // RMSNorm statistics of the fp32 rows the split down projection leaves
 // (see gemm_down_residual): the split outputs are first replaced by the sum
 // of their slices, in slice order.
-hipError_t launch_row_rms_split(float *x, int n, int h, float eps, float *r, DownSplit sp, hipStream_t stream);
+hipError_t launch_row_rms_split(float *x, int n, int h, float eps, float *r, SplitTail sp, hipStream_t stream);
 
 // Apply the row statistics, a gain and a bias: x_hat = (x - mu[n]) * r[n]
 // (mu == NULL: no centring; r == NULL: no scale), z = x_hat * gain + bias
@@ -88,9 +90,9 @@ hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *par
 
 // RMSNorm backward through the exit norm of an MLP exit:
 //   dz_hat = dZ * gain,  z_hat = y * r,  dY = r (dz_hat - z_hat mean_j(dz_hat z_hat)),
-// with dZ the sum of `splits` partial products zstride floats apart.
+// with dZ as gemm_dz leaves it for the split sp (its slices added in order).
 hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const float *r, const void *gain,
-                           int n, int h, void *dy, hipStream_t stream, int splits = 1, int64_t zstride = 0);
+                           int n, int h, void *dy, hipStream_t stream, SplitTail sp = SplitTail{0, 0, 1});
 
 
 // ------------------------------------------------------------------ GEMMs
@@ -123,17 +125,16 @@ int split_kchunk(int K, int splits);
 // Y[n][h] = X + A W_down^T  (fp32 out).  With sp.splits > 1 the outputs in
 // sp's region are sp.splits partial sums over slices of I: slice 0 (which
 // adds X) in place, slice z at Y + z n h, so Y holds splits n h floats;
-// launch_row_rms_split with the same split adds them up.  down_split: the
-// split for a shape.
-DownSplit down_split(bool f32, int n, int h, int inter);
+// launch_row_rms_split with the same split adds them up.
+// split_tail: the split for n tokens by h features over a sum of depth K (a
+// shape-only rule that simulates the dispatch of a few candidates).
+SplitTail split_tail(bool f32, int n, int h, int K);
 hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, const void *x, int n,
-                              int h, int inter, float *y, hipStream_t stream, DownSplit sp = DownSplit{0, 0, 1});
-// dZ[n][h] = G W_out with G stored transposed [V][ldn]  (fp32 out), as
-// `splits` partial sums over slices of the vocabulary, n*h floats apart
-// (dz_splits: the count for a shape; the buffer holds that many slices).
-int dz_splits(bool f32, int ldn, int h, int vocab);
+                              int h, int inter, float *y, hipStream_t stream, SplitTail sp = SplitTail{0, 0, 1});
+// dZ[n][h] = G W_out with G stored transposed [V][ldn]  (fp32 out), with
+// the split sp of its vocabulary sum (the buffer holds sp.splits n h floats).
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab,
-                   float *dz, hipStream_t stream, int splits = 1);
+                   float *dz, hipStream_t stream, SplitTail sp = SplitTail{0, 0, 1});
 // One launch of two independent products of the MLP backward:
 //   dA = dY W_down with the SwiGLU backward epilogue (dH_g, dH_u), and
 //   dW_down[h][I] (=|+=) dY^T A.

@@ -116,12 +116,13 @@ SMALL_CASES = [
     # M of dW_out), and 8192 for an MLP exit (the norm backward's limit)
     ("norm_max_hidden", W.EXIT_NORM, 40, 32768, 200, 0, "bf16", False),
     ("mlp_max_hidden", W.EXIT_MLP, 96, 8192, 300, 256, "bf16", False),
-    # the down projection with a split-K tail: 256 whole-K tiles (tokens
-    # 0-2047) plus the last 152 tokens as four partial sums over I; then
-    # features 0-5375 whole and the last 64 features of every token as four
-    # partial sums over a ragged I (mlp_multi_tile: all outputs as two)
-    ("mlp_split_tokens", W.EXIT_MLP, 2200, 8192, 300, 1024, "bf16", False),
-    ("mlp_split_features", W.EXIT_MLP, 3000, 5440, 300, 1088, "bf16", False),
+    # the down projection and dZ with a split-K tail: 256 whole-K tiles
+    # (tokens 0-2047) plus the last 152 tokens as four partial sums over I
+    # (over V for dZ); then features 0-5375 whole and the last 64 features of
+    # every token as four partial sums over a ragged I and V
+    # (mlp_multi_tile: all outputs as two, and dZ as four)
+    ("mlp_split_tokens", W.EXIT_MLP, 2200, 8192, 1024, 1024, "bf16", False),
+    ("mlp_split_features", W.EXIT_MLP, 3000, 5440, 1088, 1088, "bf16", False),
     # the most tokens and the largest vocabulary the ABI accepts (2^20 each):
     # a dW_out product with K = 2^20 in one tile, and 16384 softmax slices
     ("norm_max_tokens", W.EXIT_NORM, 1 << 20, 64, 40, 0, "bf16", False),
