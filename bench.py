@@ -203,8 +203,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs the exit-head step on one GPU only; --gpus {args.gpus} "
-              "is not supported (how the step would shard is described in DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: the exit-head step runs on one GPU only; --gpus {args.gpus} is not supported",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
