@@ -688,8 +688,8 @@ hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const floa
 
 
 // ------------------------------------------------------------------ GEMMs
-// bf16 GEMMs whose operands are both K-major take the 256 x 256 tile; the
-// others (fp32, or a transposed operand) the 128 x 128 tile.
+// bf16 GEMMs take the 256 x 256 tile (either operand K-major or MN-major),
+// fp32 GEMMs the 128 x 128 tile.
 template <typename T, bool AK, bool BKM, class Epi>
 hipError_t run_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Params &ep, hipStream_t stream) {
   if constexpr (std::is_same<T, bf16_t>::value)
