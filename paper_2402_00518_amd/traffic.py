@@ -28,12 +28,14 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
-# Profiling label -> substring of the demangled kernel name (one launch per
-# exit and step each).
+# Profiling label -> substring(s) of the demangled kernel name (one launch
+# per exit and step each; a tuple lists the alternatives, e.g. with and
+# without a split-K tail).
 LABEL_KERNELS = {
     "logits + softmax partials": "ee::EpiLogits<",
     "output-matrix gradient": "gemm_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
-    "dZ": "gemm_kernel<unsigned short, false, false, ee::EpiStoreF32<",
+    "dZ": ("gemm_kernel<unsigned short, false, false, ee::EpiStoreF32<",
+           "gemm_pair_kernel<unsigned short, false, false, ee::EpiStoreF32<"),
     "gate and up gradients": "gemm_pair_kernel<unsigned short, false, false, ee::EpiWeightGrad<",
     "gate projection": "ee::EpiStore<",
     "up projection + swiglu": "ee::EpiSwiGLU<",
@@ -81,7 +83,8 @@ def per_label(rows):
     acc = defaultdict(list)
     for _, name, v in rows:
         for label, pat in LABEL_KERNELS.items():
-            if pat in name:
+            pats = pat if isinstance(pat, tuple) else (pat,)
+            if any(q in name for q in pats):
                 acc[label].append(v)
     return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
 
