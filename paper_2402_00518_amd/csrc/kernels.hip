@@ -416,19 +416,21 @@ __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
   }
 }
 
-// In-place seed: each thread owns 8 consecutive tokens of 16 vocab rows (one
-// vocab tile).  coef = s_n exp(m_tile - LSE_n) turns the stored
-// exp(S - m_tile) into s_n softmax(S); the target entry loses s_n.
+// In-place seed: each thread owns 8 consecutive tokens of kSeedRows vocab
+// rows, taken 16 at a time.  coef = s_n exp(m_tile - LSE_n) turns the stored
+// exp(S - m_tile) into s_n softmax(S); the target entry loses s_n.  The
+// coefficients are recomputed only where a group of 16 rows starts a new
+// vocab tile (once per block when the tiles are at least kSeedRows wide).
+constexpr int kSeedRows = 64;
 template <typename T>
 __global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, const float *lse,
                                                    const float *sn, const int32_t *targets, int n,
                                                    int ldn, int vocab, int vtile, float *gsum_part) {
-  __shared__ float red[16][4];
+  __shared__ float red[kSeedRows][4];
   const int c0 = blockIdx.y * 2048 + threadIdx.x * 8;
   if (gsum_part == nullptr && c0 >= ldn) return;
-  const int v0 = blockIdx.x * 16;
-  const int tile = v0 / vtile;
-  float cf[8], s[8];
+  const int vb = blockIdx.x * kSeedRows;
+  float cf[8], s[8], lz[8];
   int yy[8];
   bool ok[8];
 #pragma unroll
@@ -436,46 +438,61 @@ __global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, co
     const int c = c0 + e;
     ok[e] = c < n;
     s[e] = ok[e] ? sn[c] : 0.0f;
-    cf[e] = ok[e] ? s[e] * expf(part_m[static_cast<int64_t>(tile) * ldn + c] - lse[c]) : 0.0f;
+    lz[e] = ok[e] ? lse[c] : 0.0f;
     yy[e] = ok[e] ? targets[c] : -1;
   }
-  const int rows = min(16, vocab - v0);
-  // Issue every row's load before the first store (raw 16- or 32-byte
-  // vectors; converted at use).
-  constexpr int VEC = 8 * sizeof(T) / 16;  // 16-byte vectors per 8 values
-  u32x4_t raw[16][VEC];
+  int tile = -1;
   const int cl = min(c0, ldn - 8);  // threads past ldn (kept for the row sums) re-read the last chunk
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const u32x4_t *src = reinterpret_cast<const u32x4_t *>(P + static_cast<int64_t>(v0 + min(r, rows - 1)) * ldn + cl);
-#pragma unroll
-    for (int q = 0; q < VEC; ++q) raw[r][q] = src[q];
-  }
-  float rsum[16];
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    float p[8], g[8];
-    load_f32<8>(reinterpret_cast<const T *>(raw[r]), p);
-    rsum[r] = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      g[e] = ok[e] ? p[e] * cf[e] - (yy[e] == v0 + r ? s[e] : 0.0f) : 0.0f;
-      rsum[r] += g[e];
-    }
-    if (r < rows && c0 < ldn) store_f32<8>(P + static_cast<int64_t>(v0 + r) * ldn + c0, g);
-  }
-  // Row sums of G over this block's tokens (LayerNorm bias gradient): fp32,
-  // fixed order (wave sums, then the 4 waves in order).
-  if (gsum_part == nullptr) return;
+  constexpr int VEC = 8 * sizeof(T) / 16;  // 16-byte vectors per 8 values
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const float t = warp_sum(rsum[r]);
-    if (lane == 0) red[r][wave] = t;
+  for (int b = 0; b < kSeedRows / 16; ++b) {
+    const int v0 = vb + 16 * b;
+    const int rows = min(16, vocab - v0);
+    if (rows <= 0) break;  // uniform: past the vocabulary
+    if (v0 / vtile != tile) {
+      tile = v0 / vtile;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        cf[e] = ok[e] ? s[e] * expf(part_m[static_cast<int64_t>(tile) * ldn + c0 + e] - lz[e]) : 0.0f;
+    }
+    // Issue every row's load before the first store (raw 16- or 32-byte
+    // vectors; converted at use).
+    u32x4_t raw[16][VEC];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const u32x4_t *src = reinterpret_cast<const u32x4_t *>(P + static_cast<int64_t>(v0 + min(r, rows - 1)) * ldn + cl);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) raw[r][q] = src[q];
+    }
+    float rsum[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float p[8], g[8];
+      load_f32<8>(reinterpret_cast<const T *>(raw[r]), p);
+      rsum[r] = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        g[e] = ok[e] ? p[e] * cf[e] - (yy[e] == v0 + r ? s[e] : 0.0f) : 0.0f;
+        rsum[r] += g[e];
+      }
+      if (r < rows && c0 < ldn) store_f32<8>(P + static_cast<int64_t>(v0 + r) * ldn + c0, g);
+    }
+    // Row sums of G over this block's tokens (LayerNorm bias gradient):
+    // fp32, fixed order (wave sums, then the 4 waves in order below).
+    if (gsum_part != nullptr) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float t = warp_sum(rsum[r]);
+        if (lane == 0) red[16 * b + r][wave] = t;
+      }
+    }
   }
+  if (gsum_part == nullptr) return;
   __syncthreads();
-  if (threadIdx.x < rows)
-    gsum_part[static_cast<int64_t>(blockIdx.y) * vocab + v0 + threadIdx.x] =
+  const int rows_all = min(kSeedRows, vocab - vb);
+  if (static_cast<int>(threadIdx.x) < rows_all)
+    gsum_part[static_cast<int64_t>(blockIdx.y) * vocab + vb + threadIdx.x] =
         ((red[threadIdx.x][0] + red[threadIdx.x][1]) + red[threadIdx.x][2]) + red[threadIdx.x][3];
 }
 
@@ -643,7 +660,7 @@ int seed_chunks(int ldn) { return cdiv(ldn, 2048); }
 hipError_t launch_seed(bool f32, void *P, const float *part_m, const float *lse, const float *sn,
                        const int32_t *targets, int n, int ldn, int vocab, int vtile, hipStream_t stream,
                        float *gsum_part) {
-  const dim3 grid(cdiv(vocab, 16), seed_chunks(ldn));
+  const dim3 grid(cdiv(vocab, kSeedRows), seed_chunks(ldn));
   EE_DISPATCH(f32, hipLaunchKernelGGL(seed_kernel<T>, grid, dim3(256), 0, stream, static_cast<T *>(P), part_m,
                                       lse, sn, targets, n, ldn, vocab, vtile, gsum_part));
   return hipGetLastError();
