@@ -7,7 +7,7 @@
 // a wide W past 8 token rows, so that each token fragment serves two row
 // groups and the token rows' share of the loads halves); each of its waves takes a share
 // of K and reads its rows straight into MFMA A fragments (16 bytes of K per
-// lane), 8 fragments per row group in flight per lane, with no LDS staging;
+// lane), 12 fragments per row group in flight per lane, with no LDS staging;
 // the token rows come from L2 as B fragments (tokens past B re-read row B-1
 // and their outputs are dropped).  The waves' partial sums meet in LDS in a
 // fixed order and the first wave runs the epilogue.  Splitting K gives about
@@ -41,7 +41,7 @@ constexpr int kDecWavesMax = 16;
 __host__ __device__ constexpr int dec_waves(int row_blocks) {
   return row_blocks >= 512 ? 4 : (row_blocks >= 256 ? 8 : 16);
 }
-constexpr int kDecGroup = 8;    // fragment loads per operand per lane in flight
+constexpr int kDecGroup = 12;   // fragment loads per operand per lane in flight (8 and 16 measured slower)
 
 template <typename T> struct DecFrag;
 // bf16: a 16-byte load holds 8 values of K; one MFMA consumes 16 (two lane halves).

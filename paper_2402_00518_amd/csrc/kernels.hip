@@ -420,8 +420,8 @@ __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
 // rows, taken 16 at a time.  coef = s_n exp(m_tile - LSE_n) turns the stored
 // exp(S - m_tile) into s_n softmax(S); the target entry loses s_n.  The
 // coefficients are recomputed only where a group of 16 rows starts a new
-// vocab tile (once per block when the tiles are at least kSeedRows wide).
-constexpr int kSeedRows = 64;
+// vocab tile (once per 64-row softmax slice).
+constexpr int kSeedRows = 128;
 template <typename T>
 __global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, const float *lse,
                                                    const float *sn, const int32_t *targets, int n,
