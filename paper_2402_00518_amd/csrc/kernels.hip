@@ -479,13 +479,24 @@ __global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, co
       if (r < rows && c0 < ldn) store_f32<8>(P + static_cast<int64_t>(v0 + r) * ldn + c0, g);
     }
     // Row sums of G over this block's tokens (LayerNorm bias gradient):
-    // fp32, fixed order (wave sums, then the 4 waves in order below).
+    // fp32, fixed order.  A reduce-scatter over the wave leaves lane l with
+    // row l % 16 after four halving exchanges (bits 3..0 of the lane) and
+    // two full ones (16, 32): 17 shuffles instead of 16 wave sums; then the
+    // 4 waves in order below.
     if (gsum_part != nullptr) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float t = warp_sum(rsum[r]);
-        if (lane == 0) red[16 * b + r][wave] = t;
-      }
+      static_for<4>([&](auto st) EE_ALWAYS_INLINE {
+        constexpr int S = decltype(st)::value, BIT = 3 - S, H = 8 >> S;
+        const bool hi = (lane >> BIT) & 1;
+        static_for<H>([&](auto kk) EE_ALWAYS_INLINE {
+          constexpr int K = decltype(kk)::value;
+          const float send = hi ? rsum[K] : rsum[K + H];
+          const float keep = hi ? rsum[K + H] : rsum[K];
+          rsum[K] = keep + __shfl_xor(send, 1 << BIT);
+        });
+      });
+      rsum[0] += __shfl_xor(rsum[0], 16);
+      rsum[0] += __shfl_xor(rsum[0], 32);
+      if (lane < 16) red[16 * b + lane][wave] = rsum[0];
     }
   }
   if (gsum_part == nullptr) return;
