@@ -269,17 +269,28 @@ struct DecLogits {
   }
 };
 
-// One block of 256 threads per token: combine the tiles' partials.
+// One block of 256 threads per token: combine the tiles' partials.  Each
+// thread scans every 256th tile, then the waves combine by shuffles and the
+// four waves through LDS (two barriers per reduction).
+__device__ __forceinline__ void argmax_merge(float &m, int &t, float om, int ot) {
+  // the larger maximum, the lower tile on a tie; a thread that saw no tile
+  // (t < 0) takes any other, and a NaN never displaces a tile already seen
+  if (ot >= 0 && (t < 0 || om > m || (om == m && ot < t))) {
+    m = om;
+    t = ot;
+  }
+}
+
 __global__ __launch_bounds__(256) void decide_kernel(const float *part_m, const float *part_l,
                                                      const int32_t *part_arg, int tiles, int B, float threshold,
                                                      int32_t *token, float *confidence, int32_t *exit_flag) {
-  __shared__ float sm[256];
-  __shared__ int st[256];
-  __shared__ float sl[256];
-  const int j = blockIdx.x, tid = threadIdx.x;
-  // max over tiles, and the lowest tile reaching it (its arg is the lowest id)
-  // t_best < 0: no tile seen.  The first tile a thread sees is always taken,
-  // so the result is a valid tile even when no maximum compares (NaN).
+  __shared__ float sm[4];
+  __shared__ int st[4];
+  __shared__ float sl[4];
+  const int j = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // max over tiles, and the lowest tile reaching it; the first tile a thread
+  // sees is always taken, so the result is a valid tile even when no maximum
+  // compares (NaN)
   float m = -INFINITY;
   int t_best = -1;
   for (int t = tid; t < tiles; t += 256) {
@@ -289,35 +300,25 @@ __global__ __launch_bounds__(256) void decide_kernel(const float *part_m, const 
       t_best = t;
     }
   }
-  sm[tid] = m;
-  st[tid] = t_best;
-  __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s) {
-      const float om = sm[tid + s];
-      const int ot = st[tid + s];
-      if (ot >= 0 && (st[tid] < 0 || om > sm[tid] || (om == sm[tid] && ot < st[tid]))) {
-        sm[tid] = om;
-        st[tid] = ot;
-      }
-    }
-    __syncthreads();
+  for (int o = 1; o < 64; o <<= 1) argmax_merge(m, t_best, __shfl_xor(m, o), __shfl_xor(t_best, o));
+  if (lane == 0) {
+    sm[wave] = m;
+    st[wave] = t_best;
   }
-  const float mx = sm[0];
-  const int tb = st[0];
+  __syncthreads();
+  float mx = sm[0];
+  int tb = st[0];
+  for (int w = 1; w < 4; ++w) argmax_merge(mx, tb, sm[w], st[w]);
   float l = 0.0f;
   for (int t = tid; t < tiles; t += 256) {
     const int64_t o = static_cast<int64_t>(t) * B + j;
     l += part_l[o] * __expf(part_m[o] - mx);
   }
-  sl[tid] = l;
+  l = warp_sum(l);
+  if (lane == 0) sl[wave] = l;
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s) sl[tid] += sl[tid + s];
-    __syncthreads();
-  }
   if (tid == 0) {
-    const float conf = 1.0f / sl[0];
+    const float conf = 1.0f / ((sl[0] + sl[1]) + (sl[2] + sl[3]));
     token[j] = part_arg[static_cast<int64_t>(tb) * B + j];
     confidence[j] = conf;
     exit_flag[j] = conf > threshold ? 1 : 0;
