@@ -27,6 +27,9 @@ METRIC = "exit-head fwd+bwd tokens/sec at h=4096,V=32000; % bf16 MFMA peak"
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense MFMA
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+# launch name -> label of the counter-measured traffic of the same kernel
+TRAFFIC_LABEL = {"exit norm rms": "norm statistics", "mlp pre-norm rms": "norm statistics",
+                 "exit norm apply": "norm apply", "mlp pre-norm apply": "norm apply"}
 
 
 def log(msg):
@@ -56,6 +59,42 @@ def step_flops(w):
     N, h, V, I = w.n_tokens, w.hidden, w.vocab, w.intermediate
     per = 14 * h * I + 6 * h * V if w.kind == 2 else 4 * h * V
     return per * N * w.n_exits
+
+
+def side_pass_bytes(w, name):
+    """Algorithmic HBM bytes of one launch of the step's HBM-bound passes:
+    what each pass must read and write at least (norm statistics: read the
+    rows; norm apply: read the rows, write Z and the token-contiguous copy of
+    x_hat, or U and U_hat; cross-entropy reduce: read the softmax partials;
+    seed: read P and write G in place)."""
+    N, h, V, I = w.n_tokens, w.hidden, w.vocab, w.intermediate
+    es = 2 if w.dtype == "bf16" else 4
+    ldn = (N + 63) // 64 * 64
+    slices = (V + 63) // 64
+    table = {
+        "exit norm rms": N * h * (4 if w.kind == 2 else es) + N * 4,
+        "mlp pre-norm rms": N * h * es + N * 4,
+        "exit norm apply": N * h * (4 if w.kind == 2 else es) + N * 4 + N * h * es + h * ldn * es,
+        "mlp pre-norm apply": N * h * es + N * 4 + 2 * N * h * es,
+        "cross-entropy reduce": 2 * slices * ldn * 4 + 3 * N * 4,
+        "logit seed": 2 * V * ldn * es + slices * ldn * 4,
+        "exit norm backward": 2 * N * h * 4 + N * h * es,
+    }
+    return table.get(name)
+
+
+def profile_figure(workload, kernel):
+    """Mean duration (ms) of a kernel in the committed rocprofv3 kernel-trace
+    summary of this workload, if it was taken on the current sources."""
+    from paper_2402_00518_amd.traffic import source_digest
+    try:
+        data = json.load(open(os.path.join(ROOT, "profiles", "kernel_times.json")))
+    except (OSError, ValueError):
+        return None
+    rec = data.get(workload, {}).get(kernel)
+    if not rec or rec.get("source_digest") != source_digest():
+        return None
+    return rec
 
 
 def measured_traffic(workload, kernel):
@@ -157,16 +196,29 @@ def copy_calibration(mib, copies=3):
     log(f"copy calibration: {copies} copies of {mib} MiB")
 
 
+def cpu_model():
+    """The host CPU's model name, from /proc/cpuinfo."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(batch, sample_tokens, min_seconds=10.0):
+    """The fp64 oracle on the host cores this process may run on, BLAS
+    threads set to that count."""
     import numpy as np
     import oracle as O
     import workloads as W
+    cores = len(os.sched_getaffinity(0))
     try:
-        from threadpoolctl import threadpool_info
-        threads = max((p.get("num_threads", 1) for p in threadpool_info()
-                       if p.get("user_api") == "blas"), default=1)
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores, user_api="blas")
     except Exception:
-        threads = 1
+        limiter = None
     w = batch.workload
     n = w.n_tokens if sample_tokens <= 0 else min(sample_tokens, w.n_tokens)
     exits = O.exits_from_batch(batch)
@@ -179,7 +231,17 @@ def cpu_baseline(batch, sample_tokens, min_seconds=10.0):
         O.multi_exit_step(exits, xs, y, list(w.exit_weights))
         dt += time.perf_counter() - t0
         reps += 1
-    return {"value": reps * n / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+    threads = cores
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"),
+                      default=cores)
+    except Exception:
+        pass
+    if limiter is not None:
+        limiter.restore_original_limits()
+    return {"value": reps * n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "cpu_model": cpu_model(), "blas_threads": int(threads),
             "sample": f"first {n} of {w.n_tokens} tokens, all {w.n_exits} exit(s), full h={w.hidden} "
                       f"V={w.vocab}; fp64 numpy forward+backward, {reps} step(s) in {dt:.1f} s",
             "seconds": dt}
@@ -283,7 +345,23 @@ def main():
                                "unit": "TFLOP/s", "frac": ach / peak,
                                "traffic": measured_traffic(w.name, dom),
                                "flops_per_launch": f, "avg_ms": kernels[dom]["avg_ms"]}
+            prof = profile_figure(w.name, dom)
+            if prof is not None:
+                # the same kernel in the committed rocprofv3 summary (another run)
+                pa = f / (prof["avg_us"] / 1e6) / 1e12
+                out["roofline"].update({"profile_avg_ms": prof["avg_us"] / 1e3, "profile_achieved": pa,
+                                        "profile_frac": pa / peak, "profile_file": prof["file"]})
         log(f"dominant kernel {dom}: {kernels[dom]['avg_ms']:.4f} ms")
+        side = {}
+        for k, rec in kernels.items():
+            nb = side_pass_bytes(w, k)
+            if nb is None:
+                continue
+            gbps = nb / (rec["avg_ms"] / 1e3) / 1e9
+            side[k] = {"avg_ms": rec["avg_ms"], "algorithmic_bytes": nb, "achieved_GBps": gbps,
+                       "peak_GBps": PEAK_HBM_GBS, "frac": gbps / PEAK_HBM_GBS, "bound": "hbm",
+                       "traffic": measured_traffic(w.name, TRAFFIC_LABEL.get(k, k))}
+        out["hbm_passes"] = side
 
     if not args.no_update_leg:
         out["adam_update"] = adam_leg(sess, args.steps, args.warmup)

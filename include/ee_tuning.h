@@ -4,10 +4,10 @@
  * EE-Tuning (arXiv 2402.00518) converts a frozen pre-trained LLM into an
  * early-exit one by attaching exit heads to intermediate hidden states and
  * tuning only those heads.  This library runs the hot part of one tuning
- * iteration (Sec. 3.2, "Computational efficiency", item 2): for every exit,
+ * iteration (Sec. 2.2, "Computational efficiency", item 2): for every exit,
  * the forward pass, the next-token loss, and the backward pass into the
  * exit's own parameters.  The backbone is frozen, so no gradient is produced
- * for the hidden states (Sec. 3.2, first paragraph).
+ * for the hidden states (Sec. 2.2, first paragraph).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -27,7 +27,7 @@
  *    device sees: the kernels never access memory with them, record the
  *    fault in the workspace, and ee_check_device_error() reports it.
  *  - Matrices are row-major.  The output embedding, an h x V matrix in the
- *    paper (Sec. 3.1, Embedding exit), is stored as W_out[V][h], the common
+ *    paper (Sec. 2.1, Embedding exit), is stored as W_out[V][h], the common
  *    checkpoint layout; it is the same matrix.
  *  - Mixed precision (EE_BF16): hidden states and weights are bf16; norms,
  *    softmax and losses run in fp32; GEMMs take bf16 operands with fp32
@@ -61,9 +61,9 @@ typedef enum ee_status {
 
 typedef enum ee_dtype { EE_F32 = 0, EE_BF16 = 1 } ee_dtype;
 
-/* Exit architectures of Sec. 3.1 ("Architectures of early exits"):
+/* Exit architectures of Sec. 2.1 ("Architectures of early exits"):
  *  EMBEDDING  logits = X W_out^T                                  (one matrix)
- *  NORM       logits = RMSNorm_gamma(X) W_out^T       (RMSNorm as in Sec. 4.2)
+ *  NORM       logits = RMSNorm_gamma(X) W_out^T       (RMSNorm as in Sec. 3.2)
  *  MLP        Y = X + SwiGLU(RMSNorm_gamma_mlp(X)) W_down^T   (pre-norm residual
  *             module, Fig. 2 caption), logits = RMSNorm_gamma(Y) W_out^T
  *  LAYER      a full Transformer layer in front of Norm: EE_ERR_UNSUPPORTED.
@@ -76,7 +76,7 @@ typedef enum ee_exit_kind {
   EE_EXIT_LAYER = 3
 } ee_exit_kind;
 
-/* Normalisation of a Norm exit (Sec. 3.1: "a LayerNorm or RMSNorm module").
+/* Normalisation of a Norm exit (Sec. 2.1: "a LayerNorm or RMSNorm module").
  *  RMS    s_hat = s (mean_j s_j^2 + eps)^(-1/2)                    (default)
  *  LAYER  s_hat = (s - mean_j s_j) (mean_j (s_j - mean)^2 + eps)^(-1/2),
  *         z = s_hat * gamma + beta, with beta optional (NULL: no bias).
@@ -85,12 +85,14 @@ typedef enum ee_norm { EE_NORM_RMS = 0, EE_NORM_LAYER = 1 } ee_norm;
 
 /* Step flags. */
 #define EE_FLAG_DYNAMIC_TOKEN_WEIGHTS 1u
-/* Appendix "Dynamic token-wise loss weighting": weight each token's NLL by
- * its detached confidence c_n = max_v softmax(S[n, :]).  Multiplies any
- * caller token weights. */
+/* Sec. 2.3 "Dynamic token-wise loss weights" (loss in Appendix A.3,
+ * "Dynamic token-wise loss weighting"): weight each token's NLL by its
+ * detached confidence c_n = max_v softmax(S[n, :]).  The paper weights by
+ * c_n alone; caller token weights, when given, multiply it (m_n = token_w[n]
+ * * c_n), so a row masked by weight 0 stays masked. */
 
 /* One exit's parameters (read-only; may alias another exit's, e.g. after
- * the "copy" initialisation of Sec. 3.1). */
+ * the "copy" initialisation of Sec. 2.1). */
 typedef struct ee_exit {
   int32_t kind;          /* ee_exit_kind                                     */
   int32_t dtype;         /* ee_dtype of the hidden states and all weights    */
@@ -126,7 +128,7 @@ typedef struct ee_exit_grads {
  * if the arguments are invalid (ee_last_error() says why). */
 size_t ee_workspace_bytes(int n_exits, const ee_exit *exits, int64_t n_tokens);
 
-/* Forward pass and loss of one exit (Sec. 2 loss; Sec. 3.1 architectures).
+/* Forward pass and loss of one exit (Sec. 2 loss; Sec. 2.1 architectures).
  *
  *   L_e = (1/N) sum_n m_n * ( logsumexp_v S[n, v] - S[n, y_n] ),
  *   S   = exit(hidden) W_out^T,
@@ -154,7 +156,7 @@ ee_status ee_head_forward_loss(const ee_exit *e, const void *hidden,
                                uint32_t flags, void *ws, size_t ws_bytes,
                                float *loss, float *row_loss, void *stream);
 
-/* Backward pass of one exit into its own parameters only (Sec. 3.2): writes
+/* Backward pass of one exit into its own parameters only (Sec. 2.2): writes
  * w_e * dL_e/dtheta_e for every parameter of the exit kind, consuming the
  * workspace a preceding ee_head_forward_loss left for the same exit and N.
  * accumulate = 0 overwrites the gradient buffers, 1 adds to them. */
@@ -162,7 +164,7 @@ ee_status ee_head_backward(const ee_exit *e, int64_t n_tokens, void *ws,
                            size_t ws_bytes, const ee_exit_grads *g,
                            int accumulate, void *stream);
 
-/* One full step over all exits (Sec. 3.2: exits are tuned independently and
+/* One full step over all exits (Sec. 2.2: exits are tuned independently and
  * their losses combine as a weighted sum, Sec. 1):
  *
  *   L = sum_e exit_weights[e] * L_e,
@@ -188,7 +190,7 @@ ee_status ee_multi_exit_step(int n_exits, const ee_exit *exits,
 ee_status ee_check_device_error(void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------- decode
- * Confidence-based exit decision at decode time (Sec. 4, "Inference":
+ * Confidence-based exit decision at decode time (Sec. 3, "Inference":
  * greedy decoding; an exit emits its most likely token as soon as the
  * maximum next-token probability there is above a threshold, and a
  * threshold of 1 disables early exits).  Forward only, for n_rows hidden
@@ -213,10 +215,11 @@ ee_status ee_exit_decide(const ee_exit *e, const void *hidden, int64_t n_rows,
                          int32_t *exit_flag, void *ws, size_t ws_bytes,
                          void *stream);
 
+
 /* ---------------------------------------------------------------- update
- * Adam update of exit parameters: the optimiser of Sec. 4 ("Tuning": Adam
+ * Adam update of exit parameters: the optimiser of Sec. 3 ("Tuning": Adam
  * with beta1 = 0.9, beta2 = 0.95, eps = 1e-5), the last part of a tuning
- * iteration (Sec. 3.2, "Computational efficiency").  For every element, in
+ * iteration (Sec. 2.2, "Computational efficiency").  For every element, in
  * fp32, with t = step:
  *
  *   m <- beta1 m + (1 - beta1) g
@@ -252,7 +255,7 @@ ee_status ee_adam_update(int n_tensors, const ee_adam_tensor *tensors, float lr,
                          float beta1, float beta2, float eps, int64_t step,
                          void *stream);
 
-/* Learning rate of update `step` (1-based) under the schedule of Sec. 4
+/* Learning rate of update `step` (1-based) under the schedule of Sec. 3
  * ("Tuning": linear warmup over a fraction of the iterations, then linear
  * decay from lr_max to lr_min).  With W = floor(warmup_fraction *
  * total_steps):  lr_max * step / W for step <= W;  lr_min + (lr_max - lr_min)

@@ -8,7 +8,8 @@ from .ee_oracle import (  # noqa: F401
     EXIT_EMBEDDING, EXIT_MLP, EXIT_NORM, Exit, ExitResult, confidence,
     exit_backward, exit_forward, exit_step, exit_step_sampled, layer_stats,
     layernorm_backward, log_sum_exp, logit_grad, multi_exit_step, norm_forward,
-    rms_inv, rmsnorm_backward, sigmoid, silu, silu_grad, softmax, token_nll,
+    rms_inv, rmsnorm_backward, row_weights, sigmoid, silu, silu_grad, softmax, token_nll,
+    CHUNK_ROWS,
 )
 
 

@@ -4,12 +4,12 @@ INFRASTRUCTURE ONLY.
 Only the tests, the smoke check and the benchmark's CPU-baseline leg import
 this module; the product path never does, and nothing here is shared with it.
 
-What it computes (EE-Tuning, arXiv 2402.00518, Sec. 4 "Inference"): decoding
+What it computes (EE-Tuning, arXiv 2402.00518, Sec. 3 "Inference"): decoding
 is greedy, and an exit emits its most likely next token as soon as the
 maximum next-token probability at that exit is above a pre-set threshold; a
 threshold of 1 disables early exits.  For each row n of the hidden states at
 one exit:
-    S_n        = exit(hidden_n) W_out^T             (exit_forward, Sec. 3.1)
+    S_n        = exit(hidden_n) W_out^T             (exit_forward, Sec. 2.1)
     token_n    = argmax_v S_n[v]                     (lowest id among ties)
     conf_n     = max_v softmax(S_n)[v] = exp(max_v S_n - logsumexp_v S_n)
     exit_n     = conf_n > threshold                  ("above": strict)

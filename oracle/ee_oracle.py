@@ -9,17 +9,18 @@ What it computes (EE-Tuning, arXiv 2402.00518):
   * Sec. 2 "Preliminaries": the autoregressive LM loss, the negative
     log-likelihood of each next token.  Targets arrive already shifted: row n
     of the hidden states predicts targets[n].
-  * Sec. 3.1 "Architectures of early exits": an exit maps a hidden state in
+  * Sec. 2.1 "Architectures of early exits": an exit maps a hidden state in
     R^h to logits in R^V.  Embedding = one h x V output matrix; Norm = a
     normalisation module in front of it; MLP = a backbone-shaped MLP in front
     of Norm.  Fig. 2's caption: modules are residual with pre-normalisation.
-    Sec. 4.2: the normalisation is RMSNorm, following Llama 2.
-  * Remark in Sec. 3.1: output matrices are untied (each exit owns W_out).
-  * Sec. 3.2: the backbone is frozen; each exit is tuned by backpropagation
+    Sec. 3.2: the normalisation is RMSNorm, following Llama 2.
+  * Remark in Sec. 2.1: output matrices are untied (each exit owns W_out).
+  * Sec. 2.2: the backbone is frozen; each exit is tuned by backpropagation
     into its own parameters only, independently of the other exits.
   * Sec. 1: exits' losses are combined as a weighted sum.
-  * Appendix "Dynamic token-wise loss weighting": each token's NLL may be
-    weighted by a detached confidence c_t, the maximum next-token probability.
+  * Sec. 2.3 "Dynamic token-wise loss weights" and Appendix A.3 "Dynamic
+    token-wise loss weighting": each token's NLL may be weighted by a
+    detached confidence c_t, the maximum next-token probability.
 
 Readings where the paper is silent (each also listed in the design notes):
   R1 loss over tokens is the MEAN over the N rows (token weights multiply,
@@ -30,10 +31,13 @@ Readings where the paper is silent (each also listed in the design notes):
      exit RMSNorm and W_out, two separate gains;
   R5 SwiGLU: A = silu(U W_g^T) * (U W_u^T), silu(t) = t sigmoid(t), no biases;
   R6 W_out is stored [V][h] (the paper's h x V matrix, transposed storage);
-  R19 LayerNorm flavour (Sec. 3.1 names LayerNorm or RMSNorm): s_hat =
+  R19 LayerNorm flavour (Sec. 2.1 names LayerNorm or RMSNorm): s_hat =
      (s - mean_j s_j) (mean_j (s_j - mean)^2 + eps)^(-1/2) (biased variance,
      eps inside the root), z = s_hat * gamma + beta with an optional bias;
-     an exit uses one normalisation type for all its norms.
+     an exit uses one normalisation type for all its norms;
+  R20 dynamic token-wise weights combined with caller token weights: the
+     two multiply, m_n = token_w[n] c_n (the paper has c_n alone; a caller
+     weight of 0 keeps a row masked).
 
 Pins (tests/test_oracle.py): a hand-worked golden example, closed forms at
 W_out = 0, central finite differences, torch autograd in fp64, pure-Python
@@ -130,7 +134,7 @@ def rmsnorm_backward(d_hat: np.ndarray, s_hat: np.ndarray, r: np.ndarray) -> np.
 # -------------------------------------------------------------- parameters
 @dataclasses.dataclass
 class Exit:
-    """One exit's parameters, float64 (Sec. 3.1 architectures)."""
+    """One exit's parameters, float64 (Sec. 2.1 architectures)."""
 
     kind: int
     w_out: np.ndarray                       # [V][h]
@@ -140,7 +144,7 @@ class Exit:
     w_up: Optional[np.ndarray] = None       # [I][h]
     w_down: Optional[np.ndarray] = None     # [h][I]
     eps: float = 1e-5
-    norm: str = "rms"                       # "rms" or "layer" (Sec. 3.1: LayerNorm or RMSNorm)
+    norm: str = "rms"                       # "rms" or "layer" (Sec. 2.1: LayerNorm or RMSNorm)
     beta: Optional[np.ndarray] = None       # [h]  LayerNorm bias of the exit norm, or None
 
     @property
@@ -180,7 +184,7 @@ def exit_forward(e: Exit, x: np.ndarray) -> Dict[str, np.ndarray]:
     else:
         s_in = x
     if e.kind in (EXIT_NORM, EXIT_MLP):
-        z_hat, r, z = norm_forward(e, s_in, e.gamma, e.beta)     # exit Norm (Sec. 3.1, 4.2)
+        z_hat, r, z = norm_forward(e, s_in, e.gamma, e.beta)     # exit Norm (Sec. 2.1, 3.2)
         f.update(r=r, z_hat=z_hat)
     else:
         z = s_in                                     # Embedding exit
@@ -214,7 +218,7 @@ def exit_backward(e: Exit, f: Dict[str, np.ndarray], g: np.ndarray) -> Dict[str,
     """Gradients of every exit parameter given the logit gradient g = dL/dS.
 
     Plain chain rule through S = Z W_out^T and the modules in front of it.
-    Nothing flows into the hidden states x (frozen backbone, Sec. 3.2).
+    Nothing flows into the hidden states x (frozen backbone, Sec. 2.2).
     """
     grads: Dict[str, np.ndarray] = {}
     grads["w_out"] = g.T @ f["z"]                    # dL/dW_out  [V][h]
@@ -248,6 +252,26 @@ def logit_grad(s: np.ndarray, y: np.ndarray, scale: np.ndarray) -> np.ndarray:
     return p * scale[:, None]
 
 
+# ------------------------------------------------------------ token weights
+def row_weights(conf: np.ndarray, token_weights: Optional[np.ndarray], r0: int, r1: int,
+                dynamic_weights: bool) -> np.ndarray:
+    """Loss weight m_n of rows r0..r1-1.
+
+    The caller's token weights (all ones when None; a zero masks a row,
+    reading R9) times, with ``dynamic_weights``, the detached confidence c_n,
+    the maximum next-token probability (Sec. 2.3 "Dynamic token-wise loss
+    weights"; Appendix A.3 gives the weighted loss -sum_t c_t log P(x_t | x_<t)).
+    The paper weights by c_t alone, i.e. all caller weights one; with caller
+    weights the two multiply (reading R20), so a masked row stays masked.
+    c_n is treated as a constant: no gradient flows through it.
+    """
+    m = np.ones(r1 - r0) if token_weights is None else \
+        np.asarray(token_weights[r0:r1], dtype=np.float64).copy()
+    if dynamic_weights:
+        m = m * conf
+    return m
+
+
 # ---------------------------------------------------------- one exit, all rows
 @dataclasses.dataclass
 class ExitResult:
@@ -264,10 +288,10 @@ def exit_step(e: Exit, x: np.ndarray, y: np.ndarray, exit_weight: float = 1.0,
               chunk: int = CHUNK_ROWS) -> ExitResult:
     """Loss L_e = (1/N) sum_n m_n nll_n and the gradients of exit_weight * L_e.
 
-    m_n = token_weights[n] (all ones when None); with ``dynamic_weights`` the
-    token weights are the detached confidences instead (Appendix, dynamic
-    token-wise loss weighting).  Rows are processed in chunks; gradients are
-    sums over chunks, which is the same triple sum reordered by rows only.
+    m_n = token_weights[n] (all ones when None); with ``dynamic_weights`` each
+    m_n is further multiplied by the detached confidence c_n (reading R20, see
+    row_weights).  Rows are processed in chunks; gradients are sums over
+    chunks, which is the same triple sum reordered by rows only.
     """
     n = x.shape[0]
     if n == 0:
@@ -283,12 +307,7 @@ def exit_step(e: Exit, x: np.ndarray, y: np.ndarray, exit_weight: float = 1.0,
         s = f["s"]
         nll = token_nll(s, y[r0:r1])
         c = confidence(s)
-        if dynamic_weights:
-            m = c
-        elif token_weights is not None:
-            m = np.asarray(token_weights[r0:r1], dtype=np.float64)
-        else:
-            m = np.ones(r1 - r0)
+        m = row_weights(c, token_weights, r0, r1, dynamic_weights)
         row_loss[r0:r1] = nll
         lse[r0:r1] = log_sum_exp(s)
         conf[r0:r1] = c
@@ -305,7 +324,7 @@ def multi_exit_step(exits: Sequence[Exit], xs: Sequence[np.ndarray], y: np.ndarr
                     dynamic_weights: bool = False):
     """All exits of one step: L = sum_e w_e L_e and each exit's gradients.
 
-    Exits are independent (Sec. 3.2): each one's gradient depends only on its
+    Exits are independent (Sec. 2.2): each one's gradient depends only on its
     own hidden states and parameters.
     """
     per = [exit_step(e, x, y, w, token_weights, dynamic_weights)
@@ -318,7 +337,7 @@ def multi_exit_step(exits: Sequence[Exit], xs: Sequence[np.ndarray], y: np.ndarr
 def exit_step_sampled(e: Exit, x: np.ndarray, y: np.ndarray, exit_weight: float,
                       v_rows: np.ndarray, i_rows: Optional[np.ndarray] = None,
                       token_weights: Optional[np.ndarray] = None,
-                      chunk: int = CHUNK_ROWS) -> Dict[str, np.ndarray]:
+                      chunk: int = CHUNK_ROWS, dynamic_weights: bool = False) -> Dict[str, np.ndarray]:
     """Loss, per-row NLL, full gains' gradients and sampled weight-gradient rows.
 
     Computes the forward for every row (the loss needs all of them), dL/dS
@@ -343,8 +362,7 @@ def exit_step_sampled(e: Exit, x: np.ndarray, y: np.ndarray, exit_weight: float,
         f = exit_forward(e, x[r0:r1])
         s = f["s"]
         nll = token_nll(s, y[r0:r1])
-        m = np.ones(r1 - r0) if token_weights is None else \
-            np.asarray(token_weights[r0:r1], dtype=np.float64)
+        m = row_weights(confidence(s), token_weights, r0, r1, dynamic_weights)
         row_loss[r0:r1] = nll
         lse[r0:r1] = log_sum_exp(s)
         total += float(np.sum(m * nll))

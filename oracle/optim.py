@@ -4,9 +4,9 @@ Only the tests, the smoke check and the benchmark's CPU-baseline leg import
 this module; the product path never does, and nothing here is shared with it.
 
 What it computes (EE-Tuning, arXiv 2402.00518):
-  * Sec. 3.2, "Computational efficiency": each tuning iteration ends with an
+  * Sec. 2.2, "Computational efficiency": each tuning iteration ends with an
     update of every exit's parameters from their gradients.
-  * Sec. 4, "Tuning": the optimiser is Adam with beta1 = 0.9, beta2 = 0.95,
+  * Sec. 3, "Tuning": the optimiser is Adam with beta1 = 0.9, beta2 = 0.95,
     eps = 1e-5, under a learning-rate schedule with linear warmup over the
     first 1% of the iterations to a maximum of 1e-4 and linear decay to a
     minimum of 1e-5.
@@ -47,7 +47,7 @@ PAPER_ITERATIONS = 40000
 
 def lr_schedule(step: int, total_steps: int, warmup_fraction: float, lr_max: float,
                 lr_min: float) -> float:
-    """Learning rate of update number `step` (1-based), Sec. 4 "Tuning" (R15)."""
+    """Learning rate of update number `step` (1-based), Sec. 3 "Tuning" (R15)."""
     warmup = int(math.floor(warmup_fraction * total_steps))
     if step <= warmup:
         return lr_max * step / warmup

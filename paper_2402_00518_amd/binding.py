@@ -285,3 +285,4 @@ def ee_exit_decide(e: EeExit, hidden, n_rows: int, threshold: float, token, conf
     s = lib().ee_exit_decide(ctypes.byref(e), ptr(hidden), n_rows, threshold, ptr(token),
                              ptr(confidence), ptr(exit_flag), ptr(ws), ws_bytes, stream)
     return _check(s, "ee_exit_decide") if check else s
+

@@ -1,4 +1,4 @@
-// Decode-time exit head (Sec. 4 "Inference": greedy decoding with a
+// Decode-time exit head (Sec. 3 "Inference": greedy decoding with a
 // confidence-based exit): a handful of rows through one exit, forward only.
 //
 // At decode the products are skinny, C[r][j] = sum_k W[r][k] Z[j][k] with

@@ -464,6 +464,39 @@ ee_status validate_rows(int64_t n) {
   return EE_OK;
 }
 
+ee_status validate_decide(const ee_exit *e, const void *hidden, int64_t n_rows, float threshold, int32_t *token,
+                          float *confidence, int32_t *exit_flag) {
+  EE_TRY(validate_exit(e, 0));
+  EE_TRY(validate_rows(n_rows));
+  if (std::isnan(threshold)) return fail(EE_ERR_SHAPE, "threshold is NaN");
+  EE_TRY(check_ptr(hidden, "hidden"));
+  EE_TRY(check_ptr(token, "token"));
+  EE_TRY(check_ptr(confidence, "confidence"));
+  EE_TRY(check_ptr(exit_flag, "exit_flag"));
+  return EE_OK;
+}
+
+// Outputs must not overlap each other, the inputs or the workspace (ws may be
+// NULL: the fixed array of ee_exit_decide_static is no caller buffer).
+ee_status check_decide_aliasing(const ee_exit &e, const void *hidden, int64_t n_rows, int32_t *token,
+                                float *confidence, int32_t *exit_flag, void *ws, size_t ws_bytes) {
+  const size_t n = static_cast<size_t>(n_rows);
+  const size_t es = e.dtype == EE_BF16 ? 2 : 4;
+  Range outs[4] = {make_range(token, n * 4, "token"), make_range(confidence, n * 4, "confidence"),
+                   make_range(exit_flag, n * 4, "exit_flag"), make_range(ws, ws_bytes, "workspace")};
+  const int n_outs = ws != nullptr ? 4 : 3;
+  Range ins[8];
+  int k = param_ranges(e, ins);
+  ins[k++] = make_range(hidden, n * static_cast<size_t>(e.hidden) * es, "hidden");
+  for (int a = 0; a < n_outs; ++a) {
+    for (int b = a + 1; b < n_outs; ++b)
+      if (overlap(outs[a], outs[b])) return fail(EE_ERR_ALIAS, "%s overlaps %s", outs[a].what, outs[b].what);
+    for (int b = 0; b < k; ++b)
+      if (overlap(outs[a], ins[b])) return fail(EE_ERR_ALIAS, "%s overlaps %s", outs[a].what, ins[b].what);
+  }
+  return EE_OK;
+}
+
 ee_status run_decide(const ee_exit &e, const void *x, int64_t n64, float threshold, int32_t *token,
                      float *confidence, int32_t *exit_flag, void *ws, hipStream_t s) {
   const DecLayout L = dec_layout(e, n64);
@@ -712,30 +745,13 @@ size_t ee_decode_workspace_bytes(const ee_exit *e, int64_t n_rows) {
 ee_status ee_exit_decide(const ee_exit *e, const void *hidden, int64_t n_rows, float threshold, int32_t *token,
                          float *confidence, int32_t *exit_flag, void *ws, size_t ws_bytes, void *stream) {
   g_last_error.clear();
-  EE_TRY(validate_exit(e, 0));
-  EE_TRY(validate_rows(n_rows));
-  if (std::isnan(threshold)) return fail(EE_ERR_SHAPE, "threshold is NaN");
-  EE_TRY(check_ptr(hidden, "hidden"));
-  EE_TRY(check_ptr(token, "token"));
-  EE_TRY(check_ptr(confidence, "confidence"));
-  EE_TRY(check_ptr(exit_flag, "exit_flag"));
+  EE_TRY(validate_decide(e, hidden, n_rows, threshold, token, confidence, exit_flag));
   EE_TRY(check_workspace(ws, ws_bytes, dec_layout(*e, n_rows).total));
-  const size_t n = static_cast<size_t>(n_rows);
-  const size_t es = e->dtype == EE_BF16 ? 2 : 4;
-  Range outs[4] = {make_range(token, n * 4, "token"), make_range(confidence, n * 4, "confidence"),
-                   make_range(exit_flag, n * 4, "exit_flag"), make_range(ws, ws_bytes, "workspace")};
-  Range ins[7];
-  int k = param_ranges(*e, ins);
-  ins[k++] = make_range(hidden, n * static_cast<size_t>(e->hidden) * es, "hidden");
-  for (int a = 0; a < 4; ++a) {
-    for (int b = a + 1; b < 4; ++b)
-      if (overlap(outs[a], outs[b])) return fail(EE_ERR_ALIAS, "%s overlaps %s", outs[a].what, outs[b].what);
-    for (int b = 0; b < k; ++b)
-      if (overlap(outs[a], ins[b])) return fail(EE_ERR_ALIAS, "%s overlaps %s", outs[a].what, ins[b].what);
-  }
+  EE_TRY(check_decide_aliasing(*e, hidden, n_rows, token, confidence, exit_flag, ws, ws_bytes));
   return run_decide(*e, hidden, n_rows, threshold, token, confidence, exit_flag, ws,
                     static_cast<hipStream_t>(stream));
 }
+
 
 ee_status ee_profile_start(void) {
   std::lock_guard<std::mutex> g(g_prof_mu);

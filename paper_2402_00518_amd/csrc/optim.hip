@@ -1,4 +1,4 @@
-// Adam update of exit parameters (Sec. 4 "Tuning": Adam, Kingma and Ba),
+// Adam update of exit parameters (Sec. 3 "Tuning": Adam, Kingma and Ba),
 // fused over up to kAdamMaxTensors tensors per launch.
 //
 // Per element, in fp32:

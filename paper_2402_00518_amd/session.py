@@ -77,6 +77,8 @@ class Session:
         ne = len(exits)
         self.loss_total = torch.zeros(1, dtype=torch.float32, device=self.device)
         self.loss_per_exit = torch.zeros(max(ne, 1), dtype=torch.float32, device=self.device)
+        # L_e of ee_head_forward_loss, one 16-byte aligned slot per exit
+        self.loss_fwd = torch.zeros(max(ne, 1), 4, dtype=torch.float32, device=self.device)
         self.row_loss = torch.zeros(self.n_tokens, dtype=torch.float32, device=self.device)
         self.opt_state: Optional[List[dict]] = None
 
@@ -103,9 +105,11 @@ class Session:
                              current_stream() if stream is None else stream)
 
     def forward(self, e: int = 0, flags: int = 0, row_loss: bool = True, stream: Optional[int] = None):
+        """ee_head_forward_loss of exit e: L_e into loss_fwd[e, 0], the per-row
+        NLL into row_loss."""
         B.ee_head_forward_loss(self.c_exits[e], self.x[e], self.targets, self.token_w,
                                self.n_tokens, self.exit_weights[e], flags, self.ws, self.ws_bytes,
-                               self.loss_per_exit[e:e + 1], self.row_loss if row_loss else None,
+                               self.loss_fwd[e, :1], self.row_loss if row_loss else None,
                                current_stream() if stream is None else stream)
 
     def backward(self, e: int = 0, accumulate: int = 0, stream: Optional[int] = None):
@@ -140,7 +144,7 @@ class Session:
 
     def update(self, step: int, lr: float, beta1: float = 0.9, beta2: float = 0.95, eps: float = 1e-5,
                stream: Optional[int] = None):
-        """One ee_adam_update over every exit parameter (Sec. 4 hyper-parameters by default)."""
+        """One ee_adam_update over every exit parameter (Sec. 3 hyper-parameters by default)."""
         if self.opt_state is None:
             self.init_optimizer()
         B.ee_adam_update(self.adam_tensors(), lr, beta1, beta2, eps, step,

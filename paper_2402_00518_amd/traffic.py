@@ -43,6 +43,18 @@ LABEL_KERNELS = {
     "dA + swiglu backward, down gradient": "ee::EpiSwiGLUBwd<",
     "logit seed": "seed_kernel",
     "cross-entropy reduce": "ce_reduce_kernel",
+    # normalisation passes: statistics and apply of the exit norm (and of the
+    # MLP pre-norm, whose input is the bf16 hidden state as well), the
+    # statistics that first add the split down projection's slices, the
+    # apply of the MLP exit norm to the fp32 residual stream, and the norm
+    # backward of the MLP exit
+    "norm statistics": "row_rms_kernel<",
+    "norm statistics (split sum)": "row_rms_split_kernel<",
+    "norm apply": "norm_apply_kernel<unsigned short, unsigned short>",
+    "norm apply (fp32 input)": "norm_apply_kernel<float, unsigned short>",
+    "exit norm backward": "norm_bwd_kernel<",
+    "gain reduce": "gain_reduce_kernel",
+    "adam update": "adam_kernel",
 }
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 

@@ -11,7 +11,7 @@ from oracle import optim as OP
 
 
 def test_schedule_paper_constants():
-    # Sec. 4 "Tuning": 40k iterations, 1% warmup to 1e-4, linear decay to 1e-5.
+    # Sec. 3 "Tuning": 40k iterations, 1% warmup to 1e-4, linear decay to 1e-5.
     T, f = OP.PAPER_ITERATIONS, OP.PAPER_WARMUP_FRACTION
     lr = lambda s: OP.lr_schedule(s, T, f, OP.PAPER_LR_MAX, OP.PAPER_LR_MIN)
     assert lr(1) == pytest.approx(1e-4 / 400, rel=1e-15)

@@ -352,6 +352,54 @@ def test_dynamic_confidence_weights():
         assert abs((lp - lm) / (2 * delta) - r.grads["w_out"][idx]) < 1e-8
 
 
+@pytest.mark.parametrize("kind", KINDS)
+def test_dynamic_weights_times_token_weights(kind):
+    """Reading R20: with caller token weights m, the dynamic weight of row n is
+    m_n c_n (c detached).  Pinned by a closed form, masking and central
+    finite differences of the loss with the product frozen."""
+    rng = np.random.default_rng(105 + kind)
+    N, h, V, I = 8, 8, 11, 12
+    e = rand_exit(kind, h, V, I, rng)
+    x = rng.standard_normal((N, h))
+    y = rng.integers(0, V, N)
+    m = rng.random(N) + 0.25
+    m[[2, 5]] = 0.0
+    # all-ones caller weights are the same as none
+    a = O.exit_step(e, x, y, dynamic_weights=True)
+    b = O.exit_step(e, x, y, token_weights=np.ones(N), dynamic_weights=True)
+    assert a.loss == b.loss
+    # uniform logits: c = 1/V for every row, so L = ln(V) mean(m) / V
+    z = O.Exit(kind=kind, w_out=np.zeros((V, h)), gamma=e.gamma, gamma_mlp=e.gamma_mlp,
+               w_gate=e.w_gate, w_up=e.w_up, w_down=e.w_down)
+    u = O.exit_step(z, x, y, token_weights=m, dynamic_weights=True)
+    assert u.loss == pytest.approx(math.log(V) * np.mean(m) / V, rel=1e-14)
+    # masked rows contribute nothing (the denominator stays N)
+    full = O.exit_step(e, x, y, 0.7, token_weights=m, dynamic_weights=True)
+    keep = m != 0
+    sub = O.exit_step(e, x[keep], y[keep], 0.7, token_weights=m[keep], dynamic_weights=True)
+    assert full.loss == pytest.approx(sub.loss * keep.sum() / N, rel=1e-13)
+    for k in e.param_names():
+        np.testing.assert_allclose(full.grads[k], sub.grads[k] * keep.sum() / N, rtol=1e-11, atol=1e-16)
+    # the loss is sum_n (m_n c_n) nll_n / N with the product held constant:
+    # central differences of that loss give the gradients (times w = 0.7)
+    frozen = m * full.conf
+    ref = O.exit_step(e, x, y, token_weights=frozen)
+    assert full.loss == pytest.approx(ref.loss, rel=1e-14)
+    assert full.loss == pytest.approx(float(np.sum(frozen * full.row_loss)) / N, rel=1e-14)
+    delta = 1e-6
+    for name in e.param_names():
+        p = getattr(e, name)
+        for idx in [tuple(rng.integers(0, s) for s in p.shape) for _ in range(3)]:
+            old = p[idx]
+            p[idx] = old + delta
+            lp = O.exit_step(e, x, y, token_weights=frozen).loss
+            p[idx] = old - delta
+            lm = O.exit_step(e, x, y, token_weights=frozen).loss
+            p[idx] = old
+            fd = 0.7 * (lp - lm) / (2 * delta)
+            assert abs(fd - full.grads[name][idx]) <= 1e-7 * max(1.0, abs(fd)), (name, idx)
+
+
 # ------------------------------------------------------------ structure
 def test_chunking_does_not_change_results():
     rng = np.random.default_rng(110)
@@ -365,16 +413,19 @@ def test_chunking_does_not_change_results():
         np.testing.assert_allclose(a.grads[k], b.grads[k], rtol=1e-12, atol=1e-16)
 
 
+@pytest.mark.parametrize("dynamic", [False, True])
 @pytest.mark.parametrize("kind", KINDS)
-def test_sampled_outputs_match_full(kind):
+def test_sampled_outputs_match_full(kind, dynamic):
     rng = np.random.default_rng(120 + kind)
     N, h, V, I = 9, 8, 14, 12
     e = rand_exit(kind, h, V, I, rng)
     x = rng.standard_normal((N, h))
     y = rng.integers(0, V, N)
-    full = O.exit_step(e, x, y, 0.5)
+    m = rng.random(N) if dynamic else None
+    full = O.exit_step(e, x, y, 0.5, token_weights=m, dynamic_weights=dynamic)
     v_rows, i_rows = np.array([0, 5, 13]), np.array([2, 11])
-    smp = O.exit_step_sampled(e, x, y, 0.5, v_rows, i_rows, chunk=4)
+    smp = O.exit_step_sampled(e, x, y, 0.5, v_rows, i_rows, chunk=4, token_weights=m,
+                              dynamic_weights=dynamic)
     assert float(smp["loss"]) == pytest.approx(full.loss, rel=1e-14)
     np.testing.assert_allclose(smp["w_out_rows"], full.grads["w_out"][v_rows], rtol=1e-12)
     if kind != O.EXIT_EMBEDDING:

@@ -5,14 +5,14 @@ formats both sides read (fp32, or bf16 bit patterns as uint16).  It holds
 none of the method's arithmetic: no norm, no projection, no softmax.  The
 HIP path and the fp64 oracle decode the very same bits.
 
-Workload shapes follow the Llama-2 models the paper tunes (Sec. 4, "Models"
+Workload shapes follow the Llama-2 models the paper tunes (Sec. 3, "Models"
 and "Tuning": batch 16 x sequence 2048, Llama 2-Chat 7B/13B/70B).  Real
 hidden states and the pre-training corpus are not available, so:
   * hidden states X[n, :] = s_n * z_n with z ~ N(0, 1) and a per-row
     lognormal(0, 0.5) scale s_n, mimicking the spread of hidden-state norms
     across tokens;
   * weights ~ N(0, 0.02^2), the usual GPT initialisation (the paper's
-    "random" init, Sec. 3.1);
+    "random" init, Sec. 2.1);
   * targets follow a truncated Zipf law P(rank k) ~ k^-1.1 over the vocab,
     mapped to token ids by a seeded permutation (natural-language token
     frequencies without clustering the frequent ids in one vocab tile).
