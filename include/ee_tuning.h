@@ -215,6 +215,29 @@ ee_status ee_exit_decide(const ee_exit *e, const void *hidden, int64_t n_rows,
                          int32_t *exit_flag, void *ws, size_t ws_bytes,
                          void *stream);
 
+/* The same decision for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): no workspace argument and nothing allocated per call.  The
+ * workspace is a fixed array of EE_STATIC_SCRATCH_BYTES (32 MiB) that the
+ * library holds on each GPU it runs on until the process ends; its device
+ * address is looked up on the first call on a device.
+ *  - Runs on the current device; `stream` must belong to it.
+ *  - EE_ERR_WORKSPACE (nothing enqueued) when ee_decode_workspace_bytes(e,
+ *    n_rows) exceeds EE_STATIC_SCRATCH_BYTES (e.g. a bf16 Norm exit with
+ *    h = 8192 and V = 32000 fits about 1100 rows).
+ *  - All calls on one GPU share its one array: calls whose work overlaps on
+ *    that GPU (other streams, or threads without an order between them)
+ *    race and their results are undefined.  Calls in order on one stream are
+ *    safe; every workspace word a call reads it has written first, so what
+ *    an earlier call left there does not matter.
+ * Arguments, other errors and results as ee_exit_decide; outputs must not
+ * overlap each other or the inputs (EE_ERR_ALIAS). */
+#define EE_STATIC_SCRATCH_BYTES ((size_t)32 << 20)
+
+ee_status ee_exit_decide_static(const ee_exit *e, const void *hidden,
+                                int64_t n_rows, float threshold,
+                                int32_t *token, float *confidence,
+                                int32_t *exit_flag, void *stream);
 
 /* ---------------------------------------------------------------- update
  * Adam update of exit parameters: the optimiser of Sec. 3 ("Tuning": Adam

@@ -46,7 +46,10 @@ EXPORTS = (
     "ee_multi_exit_step", "ee_check_device_error", "ee_status_string",
     "ee_last_error", "ee_abi_version", "ee_profile_start", "ee_profile_stop",
     "ee_adam_update", "ee_lr_schedule", "ee_decode_workspace_bytes", "ee_exit_decide",
+    "ee_exit_decide_static",
 )
+# Size of the fixed workspace array of ee_exit_decide_static, per GPU.
+EE_STATIC_SCRATCH_BYTES = 32 << 20
 
 
 class EeExit(ctypes.Structure):
@@ -136,6 +139,8 @@ def lib() -> ctypes.CDLL:
         L.ee_decode_workspace_bytes.restype = ctypes.c_size_t
         L.ee_exit_decide.argtypes = [P(EeExit), vp, i64, f32, vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.ee_exit_decide.restype = i32
+        L.ee_exit_decide_static.argtypes = [P(EeExit), vp, i64, f32, vp, vp, vp, vp]
+        L.ee_exit_decide_static.restype = i32
         _lib = L
     return _lib
 
@@ -286,3 +291,9 @@ def ee_exit_decide(e: EeExit, hidden, n_rows: int, threshold: float, token, conf
                              ptr(confidence), ptr(exit_flag), ptr(ws), ws_bytes, stream)
     return _check(s, "ee_exit_decide") if check else s
 
+
+def ee_exit_decide_static(e: EeExit, hidden, n_rows: int, threshold: float, token, confidence, exit_flag,
+                          stream, check=True) -> int:
+    s = lib().ee_exit_decide_static(ctypes.byref(e), ptr(hidden), n_rows, threshold, ptr(token),
+                                    ptr(confidence), ptr(exit_flag), stream)
+    return _check(s, "ee_exit_decide_static") if check else s

@@ -14,6 +14,13 @@
 #include "../../include/ee_tuning.h"
 #include "launch.h"
 
+// The workspace of ee_exit_decide_static: a fixed array in the library's own
+// device memory, one per GPU (it comes with the code object when the library
+// is loaded on a device and stays until the process ends).  In host code
+// `scratch` names a host-side shadow, not device memory: kernels receive the
+// device address that hipGetSymbolAddress gives for the current device.
+static __device__ __align__(256) char scratch[EE_STATIC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -259,6 +266,7 @@ struct ProfRecord {
 };
 std::mutex g_prof_mu;
 bool g_prof_on = false;
+thread_local bool g_prof_suspended = false;  // set while a call must not create events
 std::vector<ProfRecord> g_prof_records;
 std::vector<hipEvent_t> g_prof_pool;
 size_t g_prof_used = 0;
@@ -276,7 +284,7 @@ hipEvent_t prof_event() {
 #define EE_LAUNCH(name, s, call)                                         \
   do {                                                                   \
     hipEvent_t _a = nullptr, _b = nullptr;                               \
-    if (g_prof_on) {                                                     \
+    if (g_prof_on && !g_prof_suspended) {                                \
       std::lock_guard<std::mutex> _g(g_prof_mu);                         \
       _a = prof_event();                                                 \
       _b = prof_event();                                                 \
@@ -494,6 +502,33 @@ ee_status check_decide_aliasing(const ee_exit &e, const void *hidden, int64_t n_
     for (int b = 0; b < k; ++b)
       if (overlap(outs[a], ins[b])) return fail(EE_ERR_ALIAS, "%s overlaps %s", outs[a].what, ins[b].what);
   }
+  return EE_OK;
+}
+
+// ------------------------------------------- decode without allocation
+constexpr size_t kStaticScratchBytes = EE_STATIC_SCRATCH_BYTES;
+
+std::mutex g_scratch_mu;
+std::vector<void *> g_scratch_ptr;  // per device, looked up on the first call there
+
+ee_status static_scratch(void **out) {
+  int dev = 0;
+  EE_HIP(hipGetDevice(&dev), "hipGetDevice");
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (g_scratch_ptr.empty()) {
+    int count = 0;
+    EE_HIP(hipGetDeviceCount(&count), "hipGetDeviceCount");
+    g_scratch_ptr.assign(static_cast<size_t>(count > 0 ? count : 0), nullptr);
+  }
+  if (dev < 0 || static_cast<size_t>(dev) >= g_scratch_ptr.size())
+    return fail(EE_ERR_HIP, "current device %d is not one of the %zu devices", dev, g_scratch_ptr.size());
+  if (g_scratch_ptr[dev] == nullptr) {
+    void *p = nullptr;
+    EE_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (p == nullptr) return fail(EE_ERR_HIP, "hipGetSymbolAddress(scratch) gave NULL on device %d", dev);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return EE_OK;
 }
 
@@ -752,6 +787,26 @@ ee_status ee_exit_decide(const ee_exit *e, const void *hidden, int64_t n_rows, f
                     static_cast<hipStream_t>(stream));
 }
 
+ee_status ee_exit_decide_static(const ee_exit *e, const void *hidden, int64_t n_rows, float threshold,
+                                int32_t *token, float *confidence, int32_t *exit_flag, void *stream) {
+  g_last_error.clear();
+  EE_TRY(validate_decide(e, hidden, n_rows, threshold, token, confidence, exit_flag));
+  const size_t need = dec_layout(*e, n_rows).total;
+  if (need > kStaticScratchBytes)
+    return fail(EE_ERR_WORKSPACE, "ee_exit_decide_static: %lld rows of this exit need %zu bytes of workspace, "
+                "above the fixed %zu-byte array (use ee_exit_decide with a workspace)",
+                static_cast<long long>(n_rows), need, kStaticScratchBytes);
+  EE_TRY(check_decide_aliasing(*e, hidden, n_rows, token, confidence, exit_flag, nullptr, 0));
+  void *ws = nullptr;
+  EE_TRY(static_scratch(&ws));
+  // no profiling events: creating them would allocate
+  const bool was = g_prof_suspended;
+  g_prof_suspended = true;
+  const ee_status st = run_decide(*e, hidden, n_rows, threshold, token, confidence, exit_flag, ws,
+                                  static_cast<hipStream_t>(stream));
+  g_prof_suspended = was;
+  return st;
+}
 
 ee_status ee_profile_start(void) {
   std::lock_guard<std::mutex> g(g_prof_mu);

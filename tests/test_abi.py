@@ -334,6 +334,29 @@ def test_decide_rejects_bad_arguments():
     assert decide_status(bad) == B.EE_ERR_UNSUPPORTED
 
 
+def static_status(e, n=4, threshold=0.5, token=0x50_0000_0000, conf=0x51_0000_0000, flag=0x52_0000_0000,
+                  hidden=X):
+    return B.ee_exit_decide_static(e, hidden, n, threshold, token, conf, flag, None, check=False)
+
+
+def test_decide_static_rejects_before_touching_the_device():
+    """The entry point without a workspace validates like ee_exit_decide and
+    refuses calls whose workspace would not fit its fixed array; all of this
+    happens before it looks up the array or enqueues anything."""
+    e = fake_exit(h=8192, V=32000)
+    fit = max(n for n in range(1, 4096) if B.ee_decode_workspace_bytes(e, n) <= B.EE_STATIC_SCRATCH_BYTES)
+    assert fit >= 1000                                        # about 1100 rows of a 70B-shaped Norm exit
+    expect(static_status(e, n=fit + 1), B.EE_ERR_WORKSPACE, "fixed")
+    assert static_status(e, n=0) == B.EE_ERR_SHAPE
+    assert static_status(e, threshold=float("nan")) == B.EE_ERR_SHAPE
+    assert static_status(e, token=None) == B.EE_ERR_NULL
+    assert static_status(e, conf=0x51_0000_0004) == B.EE_ERR_ALIGN
+    assert static_status(e, flag=0x50_0000_0000) == B.EE_ERR_ALIAS         # flag over token
+    assert static_status(e, token=X) == B.EE_ERR_ALIAS                      # output over the hidden states
+    bad = fake_exit(); bad.kind = B.EE_EXIT_LAYER
+    assert static_status(bad) == B.EE_ERR_UNSUPPORTED
+
+
 def test_mlp_exit_hidden_limit():
     e = fake_exit(B.EE_EXIT_MLP, h=8256, I=512)
     expect(fwd(e), B.EE_ERR_SHAPE, "MLP exit needs hidden")
