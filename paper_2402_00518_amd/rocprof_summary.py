@@ -44,7 +44,7 @@ def label_of(name: str):
 
 
 def short(name: str) -> str:
-    s = name.replace("void ", "").split("(")[0]
+    s = name.replace("void ", "").replace("(anonymous namespace)::", "").split("(")[0]
     return s.replace("unsigned short", "bf16")
 
 
@@ -85,7 +85,9 @@ def cmd_trace(args):
                   f"MFMA peak; dominant kernel {r.get('kernel')} at {r.get('avg_ms', float('nan')):.4f} ms mean by "
                   f"HIP events on the launch stream ({r.get('achieved', float('nan')):.0f} TFLOP/s, "
                   f"frac {r.get('frac', float('nan')):.3f}).", ""]
-    lines += ["| kernel | calls | avg µs | min µs | max µs | % time |", "|---|---|---|---|---|---|"]
+    lines += ["All kernels of the command: the step's (warmup, timed and event-timed steps), then the",
+              "Adam update and the decode-time exit decision legs of bench.py.", "",
+              "| kernel | calls | avg µs | min µs | max µs | % time |", "|---|---|---|---|---|---|"]
     for r in rows:
         lines.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
                      f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
