@@ -198,7 +198,11 @@ struct EpiLogits {
         }
         slot_reduce_scatter<true>(mx, lane);
         wl[slot_row(I0 * 16 + lo, lane)] = mx[0];
-        __syncthreads();
+        // the rows read back below are this wave's own: a wave-scope fence
+        // suffices (the other waves go on with their parts)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         // P = exp(S - m) = exp2(S log2e - m log2e), four tokens per store; row sums
         static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
           constexpr int I = I0 + decltype(ii)::value;
