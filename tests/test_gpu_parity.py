@@ -167,6 +167,11 @@ SMALL_CASES = [
     # a dW_out product with K = 2^20 in one tile, and 16384 softmax slices
     ("norm_max_tokens", W.EXIT_NORM, 1 << 20, 64, 40, 0, "bf16", False),
     ("norm_max_vocab", W.EXIT_NORM, 64, 64, 1 << 20, 0, "bf16", False),
+    # vocabulary-wide products of several rounds of 256-wide tiles with a
+    # ragged last column of tiles (200 and 156 of 256 vocabulary ids), over
+    # one and over four (ragged) rows of tiles
+    ("norm_stagger_ragged_vocab", W.EXIT_NORM, 64, 64, 767 * 256 + 200, 0, "bf16", False),
+    ("norm_stagger_ragged_rows", W.EXIT_NORM, 1000, 64, 199 * 256 + 156, 0, "bf16", True),
 ]
 
 
