@@ -42,8 +42,7 @@ def kernel_flops(w, name):
     table = {
         "logits + softmax partials": 2 * N * h * V,
         "output-matrix gradient": 2 * N * h * V,
-        "gate projection": 2 * N * h * I,
-        "up projection + swiglu": 2 * N * h * I,
+        "gate and up projections + swiglu": 2 * 2 * N * h * I,
         "down projection + residual": 2 * N * h * I,
         "dZ": 2 * N * h * V,
         "dA + swiglu backward, down gradient": 2 * 2 * N * h * I,
@@ -65,7 +64,7 @@ def side_pass_bytes(w, name):
     """Algorithmic HBM bytes of one launch of the step's HBM-bound passes:
     what each pass must read and write at least (norm statistics: read the
     rows; norm apply: read the rows, write Z and the token-contiguous copy of
-    x_hat, or U and U_hat; cross-entropy reduce: read the softmax partials;
+    x_hat, or U and the token-contiguous copy of U_hat; cross-entropy reduce: read the softmax partials;
     seed: read P and write G in place)."""
     N, h, V, I = w.n_tokens, w.hidden, w.vocab, w.intermediate
     es = 2 if w.dtype == "bf16" else 4
@@ -75,7 +74,7 @@ def side_pass_bytes(w, name):
         "exit norm rms": N * h * (4 if w.kind == 2 else es) + N * 4,
         "mlp pre-norm rms": N * h * es + N * 4,
         "exit norm apply": N * h * (4 if w.kind == 2 else es) + N * 4 + N * h * es + h * ldn * es,
-        "mlp pre-norm apply": N * h * es + N * 4 + 2 * N * h * es,
+        "mlp pre-norm apply": N * h * es + N * 4 + N * h * es + h * ldn * es,
         "cross-entropy reduce": 2 * slices * ldn * 4 + 3 * N * 4,
         "logit seed": 2 * V * ldn * es + slices * ldn * 4,
         "exit norm backward": 2 * N * h * 4 + N * h * es,

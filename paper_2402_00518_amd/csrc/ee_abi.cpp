@@ -51,7 +51,7 @@ struct Layout {
   int64_t ldn = 0, vtiles = 0, itiles = 0;
   int vtile = 0, itile = 0;
   size_t z = 0, zht = 0, r = 0, P = 0, pm = 0, pl = 0, tgt = 0, lse = 0, sn = 0, bsum = 0, dgp = 0;
-  size_t u = 0, uhat = 0, rx = 0, hg = 0, hu = 0, act = 0, y = 0, dz = 0, dy = 0, dhg = 0, dhu = 0,
+  size_t u = 0, uhat = 0, rx = 0, hg = 0, act = 0, y = 0, dz = 0, dy = 0, dhg = 0, dhu = 0,
          dgpg = 0, dgpu = 0;
   size_t mu = 0, gsp = 0, gsum = 0, dbp = 0;  // LayerNorm mean; bias: G row sums, bias partials
   ee::SplitTail zs{0, 0, 1};                  // split-K tail of the dZ product
@@ -102,18 +102,17 @@ Layout layout(const ee_exit &e, int64_t n) {
   }
   if (e.kind == EE_EXIT_MLP) {
     L.u = take(N * h * es);
-    L.uhat = take(N * h * es);
+    L.uhat = take(h * ldn * es);  // U_hat^T, token-contiguous
     L.rx = take(ldn * 4);
-    L.hg = take(N * I * es);
-    L.hu = take(N * I * es);
+    L.hg = take(2 * N * I * es);  // (H_g, H_u) side by side per element
     L.act = take(N * I * es);
     L.ys = ee::split_tail(f32, static_cast<int>(n), static_cast<int>(h), static_cast<int>(I));
     L.y = take(static_cast<size_t>(L.ys.splits) * N * h * 4);
     L.zs = ee::split_tail(f32, static_cast<int>(n), static_cast<int>(h), static_cast<int>(V));
     L.dz = take(static_cast<size_t>(L.zs.splits) * N * h * 4);
     L.dy = take(N * h * es);
-    L.dhg = take(N * I * es);
-    L.dhu = take(N * I * es);
+    L.dhg = take(I * ldn * es);  // dH_g^T, token-contiguous
+    L.dhu = take(I * ldn * es);
     L.dgpg = take(static_cast<size_t>(L.itiles) * h * 4);
     L.dgpu = take(static_cast<size_t>(L.itiles) * h * 4);
   }
@@ -315,9 +314,9 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   if (e.kind == EE_EXIT_MLP) {
     EE_LAUNCH("mlp pre-norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.rx), s, nullptr, clear));
     EE_LAUNCH("mlp pre-norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.rx), e.gamma_mlp, n, ldn, h, at(ws, L.u),
-                                 at(ws, L.uhat), nullptr, s));
-    EE_LAUNCH("gate projection", s, ee::gemm_gate(f32, at(ws, L.u), e.w_gate, n, I, h, at(ws, L.hg), s));
-    EE_LAUNCH("up projection + swiglu", s, ee::gemm_up_swiglu(f32, at(ws, L.u), e.w_up, n, I, h, at(ws, L.hg), at(ws, L.hu), at(ws, L.act), s));
+                                 nullptr, at(ws, L.uhat), s));
+    EE_LAUNCH("gate and up projections + swiglu", s, ee::gemm_gate_up_swiglu(f32, at(ws, L.u), e.w_gate, e.w_up, n, I, h, at(ws, L.hg),
+                                                                             at(ws, L.act), s));
     EE_LAUNCH("down projection + residual", s, ee::gemm_down_residual(f32, at(ws, L.act), e.w_down, x, n, h, I, atf(ws, L.y), s, L.ys));
     EE_LAUNCH("exit norm rms", s, ee::launch_row_rms_split(atf(ws, L.y), n, h, e.rms_eps, atf(ws, L.r), L.ys, s));
     EE_LAUNCH("exit norm apply", s, ee::launch_norm_apply(true, f32, atf(ws, L.y), h, atf(ws, L.r), e.gamma, n, ldn, h, at(ws, L.z),
@@ -383,10 +382,10 @@ ee_status run_backward(const ee_exit &e, int64_t n64, void *ws, const ee_exit_gr
   EE_LAUNCH("exit norm backward", s, ee::launch_norm_bwd(f32, atf(ws, L.dz), atf(ws, L.y), atf(ws, L.r), e.gamma, n, h, at(ws, L.dy), s,
                                                          L.zs));
   EE_LAUNCH("dA + swiglu backward, down gradient", s,
-            ee::gemm_da_swiglu_dw_down(f32, at(ws, L.dy), e.w_down, n, I, h, at(ws, L.hg), at(ws, L.hu), at(ws, L.dhg),
-                                       at(ws, L.dhu), at(ws, L.act), g.d_w_down, acc, s));
+            ee::gemm_da_swiglu_dw_down(f32, at(ws, L.dy), e.w_down, n, I, h, at(ws, L.hg), at(ws, L.dhg), at(ws, L.dhu),
+                                       ldn, at(ws, L.act), g.d_w_down, acc, s));
   EE_LAUNCH("gate and up gradients", s,
-            ee::gemm_weight_grad_mn_pair(f32, at(ws, L.dhg), at(ws, L.dhu), at(ws, L.uhat), I, h, n, e.gamma_mlp, e.w_gate,
+            ee::gemm_weight_grad_kk_pair(f32, at(ws, L.dhg), at(ws, L.dhu), at(ws, L.uhat), I, h, ldn, e.gamma_mlp, e.w_gate,
                                          e.w_up, g.d_w_gate, g.d_w_up, atf(ws, L.dgpg), atf(ws, L.dgpu), acc, s));
   EE_LAUNCH("mlp gain gradient", s, ee::launch_gain_reduce(atf(ws, L.dgpg), static_cast<int>(L.itiles), atf(ws, L.dgpu),
                                 static_cast<int>(L.itiles), h, g.d_gamma_mlp, acc, s));

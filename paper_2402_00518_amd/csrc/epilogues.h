@@ -94,6 +94,25 @@ __device__ __forceinline__ void slot_reduce_scatter(float (&v)[N], int lane) {
   });
 }
 
+// Sum of 16 row slots (one 32-row block) over the 32 lanes that share them:
+// four halving exchanges (lane bits 4..1) and a full one over bit 0, after
+// which v[0] of lanes 2 s and 2 s + 1 of each half-wave is the total of
+// slot s.
+__device__ __forceinline__ void slot_reduce16(float (&v)[16], int lane) {
+  static_for<4>([&](auto st) EE_ALWAYS_INLINE {
+    constexpr int S = decltype(st)::value;
+    constexpr int BIT = 4 - S, H = 8 >> S;
+    const bool hi = (lane >> BIT) & 1;
+    static_for<H>([&](auto kk) EE_ALWAYS_INLINE {
+      constexpr int K = decltype(kk)::value;
+      const float send = hi ? v[K] : v[K + H];
+      const float keep = hi ? v[K + H] : v[K];
+      v[K] = keep + __shfl_xor(send, 1 << BIT);
+    });
+  });
+  v[0] += __shfl_xor(v[0], 1);
+}
+
 // Four consecutive elements, raw (converted at use so that a batch of loads
 // is not split by conversions waiting on each of them).
 __device__ __forceinline__ u32x2_t raw4(const bf16_t *p) { return *reinterpret_cast<const u32x2_t *>(p); }
@@ -112,16 +131,22 @@ template <typename T> using Raw4 = typename Raw4Of<T>::type;
 // vocab ids).  For every token and every WN-column slice of the vocabulary
 // (one wave's columns) it keeps the online-softmax partials
 // m = max_v S and l = sum_v exp(S - m), stores P = exp(S - m) (the only copy
-// of the logits that reaches memory) at P[v][n], four tokens per 8- or
-// 16-byte store, and captures the fp32 logit of each token's target
-// (next-token NLL, Sec. 2).  Rows are handled in parts of two blocks (32
-// slots), each reduced over the wave's columns by a reduce-scatter (one row
-// per lane) and broadcast back through the wave's own LDS rows.
+// of the logits that reaches memory) at P[v][n], tokens contiguous, and
+// captures the fp32 logit of each token's target (next-token NLL, Sec. 2).
+// Rows are handled in parts of two blocks (32 slots), each reduced over the
+// wave's columns by a reduce-scatter (one row per lane) and broadcast back
+// through the wave's own LDS rows.  A part's 64 tokens are one 128-byte
+// line of a bf16 P row: in bf16 the part's P values pass through 8 KB of
+// the wave's LDS ([64 vocab ids][64 tokens], 16-byte chunks XOR-swizzled by
+// the vocab id) and leave in whole lines, eight lanes per line (a lane's own
+// four tokens would touch 32 lines per store); fp32 P is stored directly,
+// four tokens per 16-byte store.  Token columns past M up to ldp may be
+// written with finite values (the seed zeroes them).
 template <typename T>
 struct EpiLogits {
   struct Params {
     T *P;               // [V][ldp]
-    int64_t ldp;        // padded token count (multiple of 4)
+    int64_t ldp;        // padded token count (multiple of 8)
     float *part_m;      // [V / WN][ldp]
     float *part_l;      // [V / WN][ldp]
     float *tgt;         // [ldp] target logit
@@ -131,10 +156,16 @@ struct EpiLogits {
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
     constexpr int NB = Cfg::NB, NPART = Cfg::MB / 2;  // parts of two blocks
     constexpr float kLog2e = 1.4426950408889634f;
+    constexpr bool kStage = std::is_same<T, bf16_t>::value;
+    constexpr int kStageOff = 8192;  // after the targets and the row broadcasts
+    static_assert((Cfg::BM + Cfg::THREADS / 64 * Cfg::WM) * 4 <= kStageOff, "broadcast rows fit below the staging");
+    static_assert(!kStage || (Cfg::WN == 64 && kStageOff + Cfg::THREADS / 64 * 8192 <= 2 * Cfg::STAGE_BYTES),
+                  "8 KB of staging per wave");
     const int lane = t.lane, lo = lane & 31, hw = lane >> 5;
     const int wave = t.wave_m * Cfg::WAVES_N + t.wave_n;
     int *ylds = reinterpret_cast<int *>(t.smem);                                   // [BM] tile tokens' targets
     float *wl = reinterpret_cast<float *>(t.smem) + Cfg::BM + wave * Cfg::WM;     // this wave's rows
+    char *stage = t.smem + kStageOff + wave * 8192;                               // this wave's P lines
     __syncthreads();  // every wave is past its last fragment reads
     if (threadIdx.x < Cfg::BM) {
       const int r = t.m0 + static_cast<int>(threadIdx.x);
@@ -218,7 +249,14 @@ struct EpiLogits {
                 const float x = __builtin_amdgcn_exp2f(fmaf(acc[I][j][Q * 4 + E], kLog2e, -ml[E]));
                 e4[E] = cok[j] ? x : 0.0f;
               });
-              if (cok[j] && rok) store4(pcol[j] + (I * 32 + Q * 8), e4);
+              if constexpr (kStage) {
+                // vocab id fw = j * 32 + lane % 32 of the wave, tokens 32 ii + 8 Q + 4 hw + 0..3
+                const int fw = decltype(j)::value * 32 + lo;
+                store4(reinterpret_cast<T *>(stage + fw * 128 + (((decltype(ii)::value * 4 + Q) ^ (fw & 7)) << 4) + hw * 8),
+                       e4);
+              } else if (cok[j] && rok) {
+                store4(pcol[j] + (I * 32 + Q * 8), e4);
+              }
               s4 += e4;
             });
             static_for<4>([&](auto e) EE_ALWAYS_INLINE {
@@ -226,6 +264,24 @@ struct EpiLogits {
             });
           });
         });
+        if constexpr (kStage) {
+          // the lines read back are this wave's own: a wave-scope fence suffices
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+          const int tok0 = t.m0 + t.wave_m * Cfg::WM + I0 * 32;  // the part's first token
+          static_for<8>([&](auto it) EE_ALWAYS_INLINE {
+            const int c = decltype(it)::value * 64 + lane;  // chunk: vocab id c / 8, tokens 8 (c % 8) ..
+            const int fw = c >> 3, k = c & 7;
+            const u32x4_t v = *reinterpret_cast<const u32x4_t *>(stage + fw * 128 + ((k ^ (fw & 7)) << 4));
+            const int col = cbase + fw, tok = tok0 + k * 8;
+            if (col < t.N && tok < p.ldp) *reinterpret_cast<u32x4_t *>(p.P + static_cast<int64_t>(col) * p.ldp + tok) = v;
+          });
+          // the next part overwrites the staging lines
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        }
         slot_reduce_scatter<false>(sm, lane);
         const int row = t.m0 + t.wave_m * Cfg::WM + slot_row(I0 * 16 + lo, lane);
         if (cbase < t.N && row < t.M) {
@@ -249,9 +305,13 @@ struct EpiLogits {
 // With a LayerNorm bias b (z = x_hat * gain + b), Z = X_hat * gain + 1 b^T, so
 //   dW[r][j]       += gsum[r] * b[j]               (gsum[r] = sum_n G[n][r])
 //   part_b[s][j]    = sum_{r in slice s} W[r][j] * gsum[r]   (sums to d b)
-// Rows are handled in parts of two blocks (32 slots, one row per lane after
-// the reduce-scatter); the W loads of each 32-row block are issued while the
-// previous block is processed.
+// Rows are handled one 32-row block (16 slots) at a time; its partials are
+// reduced over the wave's columns by slot_reduce16.  A block's 32 features
+// are one 128-byte line of a dW row: each block's dW values pass through 8
+// KB of the wave's LDS ([64 output rows][32 features], 16-byte chunks
+// XOR-swizzled by the row) and leave in whole lines, eight lanes per line
+// (a lane's own four features would touch 32 lines per store), after the
+// block's W loads have been consumed, so no store waits on a load.
 template <typename T>
 struct EpiWeightGrad {
   struct Params {
@@ -267,12 +327,17 @@ struct EpiWeightGrad {
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    constexpr int NB = Cfg::NB, NPART = Cfg::MB / 2;
+    constexpr int NB = Cfg::NB;
     const int lane = t.lane, lo = lane & 31, hw = lane >> 5;
     const int cbase = t.n0 + t.wave_n * Cfg::WN;
     const int64_t ct = cbase / Cfg::WN;
     const int rbase = t.m0 + t.wave_m * Cfg::WM + hw * 4;  // feature of the lane's slot 0
     const bool interior = t.m0 + Cfg::BM <= t.M && cbase + Cfg::WN <= t.N;
+    constexpr int kStageOff = 8192;  // after the gain and bias
+    static_assert(2 * Cfg::BM * 4 <= kStageOff && Cfg::WN == 64 &&
+                      kStageOff + Cfg::THREADS / 64 * 8192 <= 2 * Cfg::STAGE_BYTES,
+                  "8 KB of staging per wave");
+    char *stage = t.smem + kStageOff + (t.wave_m * Cfg::WAVES_N + t.wave_n) * 8192;  // this wave's dW lines
     // The tile's gain and bias as fp32 in LDS, so that the stores below do
     // not wait on a global load per group of four features (a line's four
     // pieces then reach L2 close together, rather than spread over several
@@ -291,13 +356,11 @@ struct EpiWeightGrad {
       int col[NB];
       bool cok[NB];
       float gs[NB];
-      float *dcol[NB];      // dW[col][rbase]: group (I, Q) adds I*32 + Q*8
-      const T *wcol[NB];    // W[col][rbase]
+      const T *wcol[NB];    // W[col][rbase]: group (I, Q) adds I*32 + Q*8
       static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
         col[j] = t.col(j);
         cok[j] = kIn || col[j] < t.N;
         const int64_t o = static_cast<int64_t>(min(col[j], t.N - 1)) * p.ldw + rbase;
-        dcol[j] = p.dW + o;
         wcol[j] = kW ? p.W + o : nullptr;
         gs[j] = kB ? p.gsum[min(col[j], t.N - 1)] : 0.0f;
       });
@@ -307,42 +370,38 @@ struct EpiWeightGrad {
         const int o = I * 32 + Q * 8;
         return kIn ? o : min(o, t.M - 4 - rbase);
       };
-      // W of one 32-row block, double-buffered: the block after the current
-      // one is always in flight (two blocks of registers, no spills).
-      Raw4<T> w[2][4][NB];
+      // W of one 32-row block, loaded as the block starts (the dW lines
+      // leave through LDS afterwards, so no store waits on these loads).
+      Raw4<T> w[4][NB];
       auto load_w = [&](auto blk) EE_ALWAYS_INLINE {
         constexpr int I = decltype(blk)::value;
-        if constexpr (kW && I < Cfg::MB) {
+        if constexpr (kW) {
           static_for<4>([&](auto q) EE_ALWAYS_INLINE {
             const int o = goff(I, decltype(q)::value);
-            static_for<NB>([&](auto j) EE_ALWAYS_INLINE { w[I % 2][decltype(q)::value][j] = raw4(wcol[j] + o); });
+            static_for<NB>([&](auto j) EE_ALWAYS_INLINE { w[decltype(q)::value][j] = raw4(wcol[j] + o); });
           });
         }
       };
-      load_w(std::integral_constant<int, 0>{});
-      static_for<NPART>([&](auto hf) EE_ALWAYS_INLINE {
-        constexpr int H = decltype(hf)::value, I0 = H * 2;
+      static_for<Cfg::MB>([&](auto blk) EE_ALWAYS_INLINE {
+        constexpr int I = decltype(blk)::value;
         __builtin_amdgcn_sched_barrier(0);
-        float dg[32], db[32];
-        static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
-          constexpr int II = decltype(ii)::value, I = I0 + II;
-          load_w(std::integral_constant<int, I + 1>{});
+        float dg[16], db[16];
+        {
+          load_w(std::integral_constant<int, I>{});
           static_for<4>([&](auto q) EE_ALWAYS_INLINE {
             constexpr int Q = decltype(q)::value;
             const int o = goff(I, Q);
-            const bool rok = kIn || rbase + I * 32 + Q * 8 < t.M;
             const int lo4 = rbase - t.m0 + o;  // tile row of the group (o clamped at the problem's edge)
             const f32x4_t g4 = kG ? *reinterpret_cast<const f32x4_t *>(gl + lo4) : f32x4_t{1.0f, 1.0f, 1.0f, 1.0f};
             const f32x4_t b4 = kB ? *reinterpret_cast<const f32x4_t *>(gl + Cfg::BM + lo4) : f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
             f32x4_t sg = {0.0f, 0.0f, 0.0f, 0.0f}, sb = {0.0f, 0.0f, 0.0f, 0.0f};
             static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
               const f32x4_t c = {acc[I][j][Q * 4], acc[I][j][Q * 4 + 1], acc[I][j][Q * 4 + 2], acc[I][j][Q * 4 + 3]};
-              f32x4_t v = c * g4;
-              if constexpr (kAcc) v += raw4(dcol[j] + o);
-              if constexpr (kB) v += gs[j] * b4;
-              if (cok[j] && rok) store4(dcol[j] + o, v);
+              // output row fw = j * 32 + lane % 32 of the wave, features 8 Q + 4 hw + 0..3 of the block
+              const int fw = decltype(j)::value * 32 + lo;
+              *reinterpret_cast<f32x4_t *>(stage + fw * 128 + (((Q * 2 + hw) ^ (fw & 7)) << 4)) = c * g4;
               if constexpr (kW) {
-                const f32x4_t wv = cvt4(w[I % 2][Q][j]);
+                const f32x4_t wv = cvt4(w[Q][j]);
                 if (cok[j]) {
                   sg += wv * c;
                   if constexpr (kB) sb += wv * gs[j];
@@ -350,17 +409,43 @@ struct EpiWeightGrad {
               }
             });
             static_for<4>([&](auto e) EE_ALWAYS_INLINE {
-              constexpr int K = II * 16 + Q * 4 + decltype(e)::value;
+              constexpr int K = Q * 4 + decltype(e)::value;
               dg[K] = sg[decltype(e)::value];
               db[K] = sb[decltype(e)::value];
             });
           });
-        });
+          // the block's lines: read back (this wave's own rows, so a
+          // wave-scope fence suffices), add what accumulates, store
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+          const int fbase = t.m0 + t.wave_m * Cfg::WM + I * 32;  // the block's first feature
+          const int fb = kIn ? fbase : min(fbase, t.M - 32);      // (M is a multiple of 32)
+          static_for<8>([&](auto it) EE_ALWAYS_INLINE {
+            // two rounds of four chunks per lane (registers)
+            if constexpr (decltype(it)::value == 4) __builtin_amdgcn_sched_barrier(0);
+            const int c = decltype(it)::value * 64 + lane;  // chunk: output row c / 8, features 4 (c % 8) ..
+            const int fw = c >> 3, k = c & 7;
+            f32x4_t v = *reinterpret_cast<const f32x4_t *>(stage + fw * 128 + ((k ^ (fw & 7)) << 4));
+            const int colw = cbase + fw;
+            float *dst = p.dW + static_cast<int64_t>(kIn ? colw : min(colw, t.N - 1)) * p.ldw + fb + k * 4;
+            if constexpr (kAcc) v += raw4(dst);
+            if constexpr (kB) {
+              const f32x4_t bb = *reinterpret_cast<const f32x4_t *>(gl + Cfg::BM + (fb - t.m0) + k * 4);
+              v += p.gsum[kIn ? colw : min(colw, t.N - 1)] * bb;
+            }
+            if (kIn || (colw < t.N && fbase < t.M)) store4(dst, v);
+          });
+          // the next block overwrites the staging rows
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        }
         if constexpr (kW) {
-          slot_reduce_scatter<false>(dg, lane);
-          if constexpr (kB) slot_reduce_scatter<false>(db, lane);
-          const int row = t.m0 + t.wave_m * Cfg::WM + slot_row(I0 * 16 + lo, lane);
-          if (cbase < t.N && row < t.M) {
+          slot_reduce16(dg, lane);
+          if constexpr (kB) slot_reduce16(db, lane);
+          const int row = t.m0 + t.wave_m * Cfg::WM + slot_row(I * 16 + (lo >> 1), lane);
+          if (cbase < t.N && row < t.M && (lo & 1) == 0) {
             p.part[ct * p.ldw + row] = dg[0];
             if constexpr (kB) p.part_b[ct * p.ldw + row] = db[0];
           }
@@ -416,23 +501,6 @@ struct EpiStoreF32 {
   }
 };
 
-// Plain store in the element type, untransposed: C[row][col] (gate
-// projection with tokens as rows: H_g[n][i]).  Lanes 0-31 of each store
-// cover 32 consecutive columns of one row.
-template <typename T>
-struct EpiStore {
-  struct Params {
-    T *C;          // [M][ldc]
-    int64_t ldc;
-  };
-  template <class Cfg>
-  __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc<Cfg>(acc, t, [&](int row, int col, int, float a) EE_ALWAYS_INLINE {
-      if (row < t.M && col < t.N) p.C[static_cast<int64_t>(row) * p.ldc + col] = from_f32<T>(a);
-    });
-  }
-};
-
 // Down projection with the residual, untransposed (rows of C are tokens,
 // columns features): Y[n][j] = X[n][j] + C[n][j]  (fp32 out; lanes 0-31 of a
 // store write one 128-byte line).  With split K, slice z of the product goes
@@ -464,65 +532,167 @@ struct EpiResidual {
   }
 };
 
-// Up projection with the SwiGLU product, untransposed (rows of C are
-// tokens): H_u = C, A = silu(H_g) * H_u.  Lanes 0-31 of each access cover 32
-// consecutive features of one token row.
+// H_g and H_u of one token and feature side by side in one word (bf16) or
+// two (fp32): what the SwiGLU backward loads per element.
+template <typename T> struct GatePair;
+template <> struct GatePair<bf16_t> {
+  using type = uint32_t;
+  __device__ __forceinline__ static type make(bf16_t g, bf16_t u) {
+    return static_cast<uint32_t>(g) | (static_cast<uint32_t>(u) << 16);
+  }
+  __device__ __forceinline__ static float g(type v) { return __uint_as_float(v << 16); }
+  __device__ __forceinline__ static float u(type v) { return __uint_as_float(v & 0xFFFF0000u); }
+};
+template <> struct GatePair<float> {
+  typedef float type __attribute__((ext_vector_type(2)));
+  __device__ __forceinline__ static type make(float g, float u) { return type{g, u}; }
+  __device__ __forceinline__ static float g(type v) { return v[0]; }
+  __device__ __forceinline__ static float u(type v) { return v[1]; }
+};
+
+// Gate and up projections as one product, with the SwiGLU product.  The B
+// operand interleaves the rows of W_gate and W_up in blocks of 32
+// (KMajorPairLoader; C has 2F columns for F features), so a lane's two
+// column blocks hold H_g and H_u of the same tokens and feature
+// f = n0 / 2 + wave_n * 32 + lane % 32.  Stores, token-major, the pair
+// (H_g, H_u) at Hgu[n][f] and A = silu(H_g) * H_u at A[n][f], with H_g
+// rounded to the element type before the SiLU (the value the backward
+// reads); lanes 0-31 of each store cover 32 consecutive features of one
+// token.
 template <typename T>
-struct EpiSwiGLU {
+struct EpiGateUp {
+  static constexpr bool kPairB = true;
+  using Pair = GatePair<T>;
   struct Params {
-    const T *Hg;
-    T *Hu;
-    T *A;
-    int64_t ld;
+    typename Pair::type *Hgu;  // [M][F]
+    T *A;                      // [M][F]
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc_loaded<Cfg>(
-        acc, t, t.M, t.N,
-        [&](int row, int col) EE_ALWAYS_INLINE { return to_f32(p.Hg[static_cast<int64_t>(row) * p.ld + col]); },
-        [&](int row, int col, int, float hu, float hg) EE_ALWAYS_INLINE {
-          if (row < t.M && col < t.N) {
-            const int64_t o = static_cast<int64_t>(row) * p.ld + col;
-            p.Hu[o] = from_f32<T>(hu);
-            p.A[o] = from_f32<T>(silu_f(hg) * hu);
-          }
-        });
+    static_assert(Cfg::NB == 2 && Cfg::WN == 64, "one 32-column block of each matrix per wave");
+    const int F = t.N / 2;
+    const int f = t.n0 / 2 + t.wave_n * 32 + (t.lane & 31);
+    if (f >= F) return;  // (no barrier follows)
+    static_for<Cfg::MB>([&](auto i) EE_ALWAYS_INLINE {
+      static_for<16>([&](auto v) EE_ALWAYS_INLINE {
+        constexpr int I = decltype(i)::value, V = decltype(v)::value;
+        const int row = t.row(I, V);
+        if (row < t.M) {
+          const int64_t o = static_cast<int64_t>(row) * F + f;
+          const T hg = from_f32<T>(acc[I][0][V]);
+          const float hu = acc[I][1][V];
+          p.Hgu[o] = Pair::make(hg, from_f32<T>(hu));
+          p.A[o] = from_f32<T>(silu_f(to_f32(hg)) * hu);
+        }
+      });
+    });
   }
 };
 
-// Backward of the SwiGLU product, untransposed (rows of C = dA = dY W_down
-// are tokens, columns features i; lanes 0-31 of each access cover 32
-// consecutive features of one token):
-//   dH_g = dA * H_u * silu'(H_g),   dH_u = dA * silu(H_g).
+// Backward of the SwiGLU product (rows of C = dA = dY W_down are tokens,
+// columns features i):
+//   dH_g = dA * H_u * silu'(H_g),   dH_u = dA * silu(H_g),
+// with (H_g, H_u) read token-major as EpiGateUp stores them (lanes 0-31 of
+// each load cover 32 consecutive features of one token) and dH_g, dH_u
+// stored transposed, [feature][ldt] with tokens contiguous: the K-major
+// operands of the gate and up weight gradients.  Token columns M..ldt-1 are
+// written as zeros.  The wave's 32-row blocks go in pairs (64 tokens = one
+// 128-byte line of a bf16 feature row): both blocks' loads, then their
+// results.  In bf16 the results pass through the wave's 16 KB of the tile's
+// LDS ([output][64 features][64 tokens], 16-byte chunks XOR-swizzled by the
+// feature), so that every global store writes whole lines, eight lanes per
+// line; a lane's own four consecutive tokens (8 bytes) would touch 32 lines
+// per store.  fp32 results (16 bytes per lane) are stored directly.
 template <typename T>
 struct EpiSwiGLUBwd {
+  using Pair = GatePair<T>;
   struct Params {
-    const T *Hg;   // [N][ld]
-    const T *Hu;
-    T *dHg;
-    T *dHu;
+    const typename Pair::type *Hgu;  // [M][ld]
+    T *dHgT;                         // [N][ldt]
+    T *dHuT;
     int64_t ld;
-  };
-  struct H2 {
-    T g, u;
+    int64_t ldt;                     // multiple of 64, >= M
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
-    for_each_acc_loaded<Cfg>(
-        acc, t, t.M, t.N,
-        [&](int row, int col) EE_ALWAYS_INLINE {
-          const int64_t o = static_cast<int64_t>(row) * p.ld + col;
-          return H2{p.Hg[o], p.Hu[o]};
-        },
-        [&](int row, int col, int, float da, H2 h) EE_ALWAYS_INLINE {
-          if (row < t.M && col < t.N) {
-            const int64_t o = static_cast<int64_t>(row) * p.ld + col;
-            float sv, sg;
-            silu_and_grad(to_f32(h.g), sv, sg);
-            p.dHg[o] = from_f32<T>(da * to_f32(h.u) * sg);
-            p.dHu[o] = from_f32<T>(da * sv);
-          }
+    constexpr int NB = Cfg::NB;
+    constexpr bool kStage = std::is_same<T, bf16_t>::value;
+    static_assert(Cfg::MB % 2 == 0, "blocks go in pairs");
+    static_assert(!kStage || (Cfg::WN == 64 && Cfg::THREADS / 64 * 16384 <= 2 * Cfg::STAGE_BYTES),
+                  "16 KB of staging per wave");
+    const int wave = t.wave_m * Cfg::WAVES_N + t.wave_n;
+    char *stage = t.smem + wave * 16384;
+    if constexpr (kStage) __syncthreads();  // every wave is past its last fragment reads
+    int col[NB];
+    static_for<NB>([&](auto j) EE_ALWAYS_INLINE { col[j] = t.col(j); });
+    static_for<Cfg::MB / 2>([&](auto pp) EE_ALWAYS_INLINE {
+      constexpr int I0 = 2 * decltype(pp)::value;
+      typename Pair::type pre[2][16][NB];
+      static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
+        static_for<16>([&](auto v) EE_ALWAYS_INLINE {
+          const int row = min(t.row(I0 + decltype(ii)::value, decltype(v)::value), t.M - 1);
+          static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
+            pre[decltype(ii)::value][decltype(v)::value][j] =
+                p.Hgu[static_cast<int64_t>(row) * p.ld + min(col[j], t.N - 1)];
+          });
         });
+      });
+      static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
+        constexpr int I = I0 + decltype(ii)::value;
+        static_for<4>([&](auto q) EE_ALWAYS_INLINE {
+          constexpr int Q = decltype(q)::value;
+          const int r0 = t.row(I, Q * 4);  // rows r0 .. r0 + 3
+          static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
+            f32x4_t dg, du;
+            static_for<4>([&](auto e) EE_ALWAYS_INLINE {
+              constexpr int E = decltype(e)::value;
+              const auto h = pre[decltype(ii)::value][Q * 4 + E][j];
+              float sv, sg;
+              silu_and_grad(Pair::g(h), sv, sg);
+              const float da = acc[I][j][Q * 4 + E];
+              const bool ok = r0 + E < t.M;
+              dg[E] = ok ? da * Pair::u(h) * sg : 0.0f;
+              du[E] = ok ? da * sv : 0.0f;
+            });
+            if constexpr (kStage) {
+              // feature fw = j * 32 + lane % 32 of the wave, tokens 32 ii + 8 Q + 4 (lane / 32) + 0..3
+              const int fw = j * 32 + (t.lane & 31);
+              const int off = fw * 128 + (((decltype(ii)::value * 4 + Q) ^ (fw & 7)) << 4) + (t.lane >> 5) * 8;
+              store4(reinterpret_cast<T *>(stage + off), dg);
+              store4(reinterpret_cast<T *>(stage + 8192 + off), du);
+            } else if (r0 < p.ldt && col[j] < t.N) {
+              const int64_t o = static_cast<int64_t>(col[j]) * p.ldt + r0;
+              store4(p.dHgT + o, dg);
+              store4(p.dHuT + o, du);
+            }
+          });
+        });
+      });
+      if constexpr (kStage) {
+        // the rows read back are this wave's own: a wave-scope fence suffices
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        const int tok0 = t.m0 + t.wave_m * Cfg::WM + I0 * 32;  // first token of the pair
+        static_for<2>([&](auto o) EE_ALWAYS_INLINE {
+          T *out = decltype(o)::value == 0 ? p.dHgT : p.dHuT;
+          static_for<8>([&](auto it) EE_ALWAYS_INLINE {
+            const int c = decltype(it)::value * 64 + t.lane;  // chunk: feature c / 8, tokens 8 (c % 8) ..
+            const int fw = c >> 3, k = c & 7;
+            const u32x4_t v =
+                *reinterpret_cast<const u32x4_t *>(stage + decltype(o)::value * 8192 + fw * 128 + ((k ^ (fw & 7)) << 4));
+            const int f = t.n0 + t.wave_n * Cfg::WN + fw;
+            const int tok = tok0 + k * 8;
+            if (f < t.N && tok < p.ldt)
+              *reinterpret_cast<u32x4_t *>(out + static_cast<int64_t>(f) * p.ldt + tok) = v;
+          });
+        });
+        // the next pair overwrites the staging rows
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      }
+    });
   }
 };
 

@@ -32,7 +32,8 @@ namespace ee {
 
 struct Operand {
   const void *ptr;
-  int64_t ld;  // elements between consecutive rows of the stored matrix
+  int64_t ld;         // elements between consecutive rows of the stored matrix
+  int64_t pair = 0;   // interleaved pair (KMajorPairLoader): bytes from the first matrix to the second
 };
 
 struct GemmShape {
@@ -125,6 +126,56 @@ struct KMajorLoader {
     });
   }
 };
+
+// K-major tile whose rows come from two matrices of equal shape, F rows
+// each (F a multiple of 32), interleaved in blocks of 32: tile-space row r
+// is row (r / 64) * 32 + r % 32 of the first matrix when (r / 32) is even,
+// of the second when it is odd.  A wave whose columns are 64 tile rows wide
+// then holds both matrices' products for the same 32 rows in its two
+// 32-column blocks (the gate and up projections of one set of features).
+// Tile rows past 2F are clamped to the last row of the second matrix.
+template <typename T, int ROWS, int THREADS, int GROUPS>
+struct KMajorPairLoader {
+  static constexpr int CH = Elem<T>::CH;
+  static constexpr int PER = ROWS * 8 / THREADS;
+  static constexpr int PG = PER / GROUPS;
+  static_assert(PER % GROUPS == 0, "stage loads must split evenly over the substeps");
+  static_assert(ROWS % 64 == 0, "the tile must hold whole 64-row pairs");
+  u32x4_t reg[PER];
+  int64_t off[PER];  // bytes from the first matrix's row row0 / 2
+
+  // row0: the tile's first tile-space row (a multiple of 64); rows: 2F.
+  __device__ __forceinline__ void init(int64_t ld, int row0, int rows, int64_t pair, int tid) {
+    static_for<PER>([&](auto i) EE_ALWAYS_INLINE {
+      const int c = tid + i * THREADS;
+      const int r = min(row0 + (c >> 3), rows - 1);   // tile-space row
+      const int f = (r >> 6) * 32 + (r & 31) - row0 / 2;  // row of its matrix, from row0 / 2
+      off[i] = (static_cast<int64_t>(f) * ld + (c & 7) * CH) * static_cast<int64_t>(sizeof(T)) +
+               (((r >> 5) & 1) ? pair : 0);
+    });
+  }
+  template <int G>
+  __device__ __forceinline__ void load(const T *base, int64_t ld, int row0, int k0) {
+    const char *panel = reinterpret_cast<const char *>(base + static_cast<int64_t>(row0 / 2) * ld + k0);
+    static_for<PG>([&](auto q) EE_ALWAYS_INLINE {
+      constexpr int i = G * PG + decltype(q)::value;
+      reg[i] = *reinterpret_cast<const u32x4_t *>(panel + off[i]);
+    });
+  }
+  template <int G>
+  __device__ __forceinline__ void store(char *lds, int tid) const {
+    static_for<PG>([&](auto q) EE_ALWAYS_INLINE {
+      constexpr int i = G * PG + decltype(q)::value;
+      const int c = tid + i * THREADS;
+      *reinterpret_cast<u32x4_t *>(lds + lds_off(c >> 3, c & 7)) = reg[i];
+    });
+  }
+};
+
+// Epilogues that take the B operand as an interleaved pair declare
+// kPairB = true.
+template <class E, class = void> struct EpiPairB : std::false_type {};
+template <class E> struct EpiPairB<E, std::void_t<decltype(E::kPairB)>> : std::bool_constant<E::kPairB> {};
 
 // MN-major tile: BK k-rows x ROWS contiguous operand rows, written
 // transposed (k contiguous) into LDS.
@@ -425,10 +476,17 @@ __device__ __forceinline__ void gemm_block(const Operand &A, const Operand &B, c
   constexpr bool kAMN = kB16 && !AK, kBMN = kB16 && !BKM;  // read with the LDS transpose
   using F = Frags<T, Cfg, kAMN, kBMN>;
   constexpr int SUB = F::SUBSTEPS;
+  constexpr bool kPair = EpiPairB<Epi>::value;
+  static_assert(!kPair || BKM, "an interleaved pair is read K-major");
   typename LoaderSel<T, AK, Cfg::BM, Cfg::THREADS, SUB, true>::type la;
-  typename LoaderSel<T, BKM, Cfg::BN, Cfg::THREADS, SUB, false>::type lb;
+  std::conditional_t<kPair, KMajorPairLoader<T, Cfg::BN, Cfg::THREADS, SUB>,
+                     typename LoaderSel<T, BKM, Cfg::BN, Cfg::THREADS, SUB, false>::type>
+      lb;
   la.init(A.ld, m0, s.M, s.K, tid);
-  lb.init(B.ld, n0, s.N, s.K, tid);
+  if constexpr (kPair)
+    lb.init(B.ld, n0, s.N, B.pair, tid);
+  else
+    lb.init(B.ld, n0, s.N, s.K, tid);
   f32x16_t acc[MB][NB];
   static_for<MB>([&](auto i) EE_ALWAYS_INLINE {
     static_for<NB>([&](auto j) EE_ALWAYS_INLINE {

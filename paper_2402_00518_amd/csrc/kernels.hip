@@ -759,37 +759,27 @@ hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, in
   return hipSuccess;
 }
 
-hipError_t gemm_weight_grad_mn_pair(bool f32, const void *g1, const void *g2, const void *xhat, int m, int h, int n,
-                                   const void *gain, const void *w1, const void *w2, float *dw1, float *dw2,
-                                   float *part1, float *part2, int accumulate, hipStream_t stream) {
+hipError_t gemm_weight_grad_kk_pair(bool f32, const void *g1_t, const void *g2_t, const void *xhat_t, int m, int h,
+                                    int ldn, const void *gain, const void *w1, const void *w2, float *dw1, float *dw2,
+                                    float *part1, float *part2, int accumulate, hipStream_t stream) {
   EE_DISPATCH(f32, {
     const T *gn = static_cast<const T *>(gain);
     typename EpiWeightGrad<T>::Params e1{dw1, h, gn, static_cast<const T *>(w1), part1, accumulate};
     typename EpiWeightGrad<T>::Params e2{dw2, h, gn, static_cast<const T *>(w2), part2, accumulate};
-    return run_gemm_pair<T, false, false, EpiWeightGrad<T>, false, false, EpiWeightGrad<T>>(
-        Operand{xhat, h}, Operand{g1, m}, GemmShape{h, m, n}, e1, Operand{xhat, h}, Operand{g2, m},
-        GemmShape{h, m, n}, e2, stream);
+    return run_gemm_pair<T, true, true, EpiWeightGrad<T>, true, true, EpiWeightGrad<T>>(
+        Operand{xhat_t, ldn}, Operand{g1_t, ldn}, GemmShape{h, m, ldn}, e1, Operand{xhat_t, ldn},
+        Operand{g2_t, ldn}, GemmShape{h, m, ldn}, e2, stream);
   });
   return hipSuccess;
 }
 
-hipError_t gemm_gate(bool f32, const void *u, const void *w_gate, int n, int inter, int h, void *hg,
-                     hipStream_t stream) {
+hipError_t gemm_gate_up_swiglu(bool f32, const void *u, const void *w_gate, const void *w_up, int n, int inter,
+                               int h, void *hgu, void *act, hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiStore<T>::Params ep{static_cast<T *>(hg), inter};
-    return run_gemm<T, true, true, EpiStore<T>>(Operand{u, h}, Operand{w_gate, h}, GemmShape{n, inter, h}, ep,
-                                                   stream);
-  });
-  return hipSuccess;
-}
-
-hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int inter, int h, const void *hg,
-                          void *hu, void *act, hipStream_t stream) {
-  EE_DISPATCH(f32, {
-    typename EpiSwiGLU<T>::Params ep{static_cast<const T *>(hg), static_cast<T *>(hu), static_cast<T *>(act),
-                                     inter};
-    return run_gemm<T, true, true, EpiSwiGLU<T>>(Operand{u, h}, Operand{w_up, h}, GemmShape{n, inter, h}, ep,
-                                                    stream);
+    typename EpiGateUp<T>::Params ep{static_cast<typename GatePair<T>::type *>(hgu), static_cast<T *>(act)};
+    const int64_t pair = static_cast<const char *>(w_up) - static_cast<const char *>(w_gate);
+    return run_gemm<T, true, true, EpiGateUp<T>>(Operand{u, h}, Operand{w_gate, h, pair},
+                                                    GemmShape{n, 2 * inter, h}, ep, stream);
   });
   return hipSuccess;
 }
@@ -929,11 +919,11 @@ hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn,
 }
 
 hipError_t gemm_da_swiglu_dw_down(bool f32, const void *dy, const void *w_down, int n, int inter, int h,
-                                 const void *hg, const void *hu, void *dhg, void *dhu, const void *act, float *dwd,
+                                 const void *hgu, void *dhg_t, void *dhu_t, int ldn, const void *act, float *dwd,
                                  int accumulate, hipStream_t stream) {
   EE_DISPATCH(f32, {
-    typename EpiSwiGLUBwd<T>::Params e1{static_cast<const T *>(hg), static_cast<const T *>(hu),
-                                        static_cast<T *>(dhg), static_cast<T *>(dhu), inter};
+    typename EpiSwiGLUBwd<T>::Params e1{static_cast<const typename GatePair<T>::type *>(hgu),
+                                        static_cast<T *>(dhg_t), static_cast<T *>(dhu_t), inter, ldn};
     typename EpiStoreF32<T>::Params e2{dwd, inter, h, accumulate};
     return run_gemm_pair<T, true, false, EpiSwiGLUBwd<T>, false, false, EpiStoreF32<T>>(
         Operand{dy, h}, Operand{w_down, inter}, GemmShape{n, inter, h}, e1, Operand{dy, h}, Operand{act, inter},

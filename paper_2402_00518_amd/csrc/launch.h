@@ -107,19 +107,20 @@ hipError_t gemm_weight_grad_kk(bool f32, const void *g_t, const void *xhat_t, in
                                const void *gain, const void *w, float *dw, float *part, int accumulate,
                                hipStream_t stream, const float *gsum = nullptr, const void *bias = nullptr,
                                float *part_b = nullptr);
-// Two such weight gradients that share x_hat and the gain, operands stored
-// row-major over tokens (g1, g2 [n][m], xhat [n][h]): the gate and up
-// gradients of the MLP exit, one launch (the second problem's tiles follow
-// the first's, filling the CUs its last round leaves idle).
-hipError_t gemm_weight_grad_mn_pair(bool f32, const void *g1, const void *g2, const void *xhat, int m, int h, int n,
-                                   const void *gain, const void *w1, const void *w2, float *dw1, float *dw2,
-                                   float *part1, float *part2, int accumulate, hipStream_t stream);
-// H_g[n][I] = U W_gate^T.
-hipError_t gemm_gate(bool f32, const void *u, const void *w_gate, int n, int inter, int h, void *hg,
-                     hipStream_t stream);
-// H_u = U W_up^T, A = silu(H_g) H_u.
-hipError_t gemm_up_swiglu(bool f32, const void *u, const void *w_up, int n, int inter, int h,
-                          const void *hg, void *hu, void *act, hipStream_t stream);
+// Two such weight gradients that share x_hat and the gain (no bias), all
+// operands token-contiguous with leading dimension ldn (g1_t, g2_t [m][ldn],
+// xhat_t [h][ldn]): the gate and up gradients of the MLP exit, one launch
+// (the second problem's tiles follow the first's, filling the CUs its last
+// round leaves idle).
+hipError_t gemm_weight_grad_kk_pair(bool f32, const void *g1_t, const void *g2_t, const void *xhat_t, int m, int h,
+                                    int ldn, const void *gain, const void *w1, const void *w2, float *dw1, float *dw2,
+                                    float *part1, float *part2, int accumulate, hipStream_t stream);
+// One product for both projections of the SwiGLU MLP (W_gate and W_up rows
+// interleaved in blocks of 32 on their way into LDS): H_g = U W_gate^T and
+// H_u = U W_up^T, stored side by side per element (hgu [n][I] pairs of the
+// element type), and A = silu(H_g) H_u [n][I].  inter: a multiple of 32.
+hipError_t gemm_gate_up_swiglu(bool f32, const void *u, const void *w_gate, const void *w_up, int n, int inter,
+                               int h, void *hgu, void *act, hipStream_t stream);
 // K values per slice when a product of depth K runs as `splits` partial sums.
 int split_kchunk(int K, int splits);
 // Y[n][h] = X + A W_down^T  (fp32 out).  With sp.splits > 1 the outputs in
@@ -136,10 +137,11 @@ hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, con
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab,
                    float *dz, hipStream_t stream, SplitTail sp = SplitTail{0, 0, 1});
 // One launch of two independent products of the MLP backward:
-//   dA = dY W_down with the SwiGLU backward epilogue (dH_g, dH_u), and
+//   dA = dY W_down with the SwiGLU backward epilogue (dH_g, dH_u, stored
+//   token-contiguous: dhg_t, dhu_t [I][ldn], columns n..ldn-1 zero), and
 //   dW_down[h][I] (=|+=) dY^T A.
 hipError_t gemm_da_swiglu_dw_down(bool f32, const void *dy, const void *w_down, int n, int inter, int h,
-                                 const void *hg, const void *hu, void *dhg, void *dhu, const void *act, float *dwd,
+                                 const void *hgu, void *dhg_t, void *dhu_t, int ldn, const void *act, float *dwd,
                                  int accumulate, hipStream_t stream);
 
 // ------------------------------------------------------------- optimizer

@@ -56,8 +56,7 @@ def gemm_flops(workload: str, label: str):
         "logits + softmax partials": 2 * N * h * V,
         "output-matrix gradient": 2 * N * h * V,
         "dZ": 2 * N * h * V,
-        "gate projection": 2 * N * h * I,
-        "up projection + swiglu": 2 * N * h * I,
+        "gate and up projections + swiglu": 4 * N * h * I,
         "down projection + residual": 2 * N * h * I,
         "dA + swiglu backward, down gradient": 4 * N * h * I,
         "gate and up gradients": 4 * N * h * I,

@@ -36,9 +36,8 @@ LABEL_KERNELS = {
     "output-matrix gradient": "gemm_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
     "dZ": ("gemm_kernel<unsigned short, false, false, ee::EpiStoreF32<",
            "gemm_pair_kernel<unsigned short, false, false, ee::EpiStoreF32<"),
-    "gate and up gradients": "gemm_pair_kernel<unsigned short, false, false, ee::EpiWeightGrad<",
-    "gate projection": "ee::EpiStore<",
-    "up projection + swiglu": "ee::EpiSwiGLU<",
+    "gate and up gradients": "gemm_pair_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
+    "gate and up projections + swiglu": "ee::EpiGateUp<",
     "down projection + residual": "ee::EpiResidual<",
     "dA + swiglu backward, down gradient": "ee::EpiSwiGLUBwd<",
     "logit seed": "seed_kernel",
