@@ -372,10 +372,28 @@ struct EpiWeightGrad {
       };
       // W of one 32-row block, loaded as the block starts (the dW lines
       // leave through LDS afterwards, so no store waits on these loads).
+      // fp32: four 16-byte loads per column, one per group of four features.
+      // bf16: two 16-byte loads per column, eight features each: in load g
+      // the half-waves take features 16 g + 8 hw .. + 7 of the block, and
+      // one exchange between the half-waves (v_permlane32_swap) leaves each
+      // lane its own four features of groups 2 g and 2 g + 1.
       Raw4<T> w[4][NB];
       auto load_w = [&](auto blk) EE_ALWAYS_INLINE {
         constexpr int I = decltype(blk)::value;
-        if constexpr (kW) {
+        if constexpr (kW && std::is_same<T, bf16_t>::value) {
+          static_for<2>([&](auto g) EE_ALWAYS_INLINE {
+            constexpr int G = decltype(g)::value;
+            // wcol includes this lane's 4 hw; edge blocks clamp into [0, M - 8]
+            const int o = kIn ? I * 32 + G * 16 + hw * 4 : min(I * 32 + G * 16 + hw * 4, t.M - 8 - rbase);
+            static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
+              const u32x4_t v = *reinterpret_cast<const u32x4_t *>(wcol[j] + o);
+              const auto s0 = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
+              const auto s1 = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
+              w[2 * G][j] = u32x2_t{s0[0], s1[0]};
+              w[2 * G + 1][j] = u32x2_t{s0[1], s1[1]};
+            });
+          });
+        } else if constexpr (kW) {
           static_for<4>([&](auto q) EE_ALWAYS_INLINE {
             const int o = goff(I, decltype(q)::value);
             static_for<NB>([&](auto j) EE_ALWAYS_INLINE { w[decltype(q)::value][j] = raw4(wcol[j] + o); });
