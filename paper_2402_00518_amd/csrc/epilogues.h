@@ -72,6 +72,22 @@ __device__ __forceinline__ int slot_row(int k, int lane) {
   return i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
 }
 
+// The first butterfly step of the reductions below, over lane bit 4, for
+// H slot pairs (K, K + H): lanes with the bit clear keep slot K, the others
+// slot K + H, each combined with its partner's value of the same slot.  One
+// v_permlane16_swap per pair exchanges exactly those two values (the
+// partner's copy of the kept slot lands in the other register), so no lane
+// selects what to send: v[K] = op(first, second) in either half.
+template <bool IsMax, int H, int N>
+__device__ __forceinline__ void slot_step_bit4(float (&v)[N]) {
+  static_for<H>([&](auto kk) EE_ALWAYS_INLINE {
+    constexpr int K = decltype(kk)::value;
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[K]), __float_as_uint(v[K + H]), false, false);
+    const float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+    v[K] = IsMax ? fmaxf(a, b) : a + b;
+  });
+}
+
 // Reduce-scatter of N row slots over the 32 lanes that share them: five
 // butterfly steps (lane bits 4..0), each halving the values a lane keeps, so
 // N/2 + N/4 + ... + N/32 shuffles instead of 5 N.  On return v[x], x < N/32,
@@ -80,8 +96,9 @@ __device__ __forceinline__ int slot_row(int k, int lane) {
 template <bool IsMax, int N>
 __device__ __forceinline__ void slot_reduce_scatter(float (&v)[N], int lane) {
   static_assert(N >= 32 && (N & (N - 1)) == 0, "slots must be a power of two >= 32");
-  static_for<5>([&](auto st) EE_ALWAYS_INLINE {
-    constexpr int S = decltype(st)::value;
+  slot_step_bit4<IsMax, N / 2>(v);
+  static_for<4>([&](auto st0) EE_ALWAYS_INLINE {
+    constexpr int S = decltype(st0)::value + 1;
     constexpr int BIT = 4 - S, H = (N >> S) / 2;
     const bool hi = (lane >> BIT) & 1;
     static_for<H>([&](auto kk) EE_ALWAYS_INLINE {
@@ -99,8 +116,9 @@ __device__ __forceinline__ void slot_reduce_scatter(float (&v)[N], int lane) {
 // which v[0] of lanes 2 s and 2 s + 1 of each half-wave is the total of
 // slot s.
 __device__ __forceinline__ void slot_reduce16(float (&v)[16], int lane) {
-  static_for<4>([&](auto st) EE_ALWAYS_INLINE {
-    constexpr int S = decltype(st)::value;
+  slot_step_bit4<false, 8>(v);
+  static_for<3>([&](auto st0) EE_ALWAYS_INLINE {
+    constexpr int S = decltype(st0)::value + 1;
     constexpr int BIT = 4 - S, H = 8 >> S;
     const bool hi = (lane >> BIT) & 1;
     static_for<H>([&](auto kk) EE_ALWAYS_INLINE {
