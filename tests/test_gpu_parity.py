@@ -373,6 +373,26 @@ def test_aliased_weights_give_identical_gradients():
         assert torch.equal(s.grads[0][k], s.grads[1][k]), k
 
 
+def test_mlp_gate_and_up_in_one_buffer():
+    """The fused gate/up product reads W_up at a byte offset from W_gate (the
+    interleaved B loader); an exit whose two projections are one buffer
+    (offset 0) must match the oracle with W_up = W_gate, gradients included
+    (d_w_gate and d_w_up stay separate outputs)."""
+    say("case: MLP exit with W_up aliasing W_gate")
+    from paper_2402_00518_amd import binding as B
+    from paper_2402_00518_amd.session import Session
+    b = small(W.EXIT_MLP, 260, 192, 900, 320, seed=61, name="gate_up_alias")
+    b.exits[0].w_up = b.exits[0].w_gate.copy()
+    s = Session.from_batch(b)
+    prm = dict(s.params[0])
+    prm["w_up"] = prm["w_gate"]
+    s.c_exits[0] = B.make_exit(W.EXIT_MLP, s.dtype, 192, 900, 320, 1e-5, **prm)
+    s.step()
+    torch.cuda.synchronize()
+    s.check_device_error()
+    compare_full(s, b, case="gate_up_alias")
+
+
 def test_out_of_range_target_is_reported():
     say("case: target outside the vocabulary")
     from paper_2402_00518_amd import binding as B
