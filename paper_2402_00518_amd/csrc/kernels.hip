@@ -287,13 +287,16 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int spli
                                                        int h, T *dy) {
   // One wave per row; the row's dZ * gain stays in registers (CH 8-wide
   // chunks per lane, h <= CH * 512) between the projection and the output,
-  // so dZ's slices are read once.
+  // so dZ's slices are read once; up to CH = 12 (h <= 6144) the row of Y
+  // stays too (else it is read again, mostly from HBM: a row is 4h bytes).
+  constexpr bool kKeepY = CH <= 12;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= n) return;
   const int64_t o = static_cast<int64_t>(row) * h;
   const float rr = r[row];
   const int f0 = row >= tok0 ? feat0 : h;  // features from f0 on are split
   float dg[CH][8];
+  float yk[kKeepY ? CH : 1][8];
   float s = 0.0f;
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
@@ -307,6 +310,7 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int spli
       for (int e = 0; e < 8; ++e) {
         dg[c][e] *= g[e];
         s += dg[c][e] * yy[e] * rr;
+        if constexpr (kKeepY) yk[c][e] = yy[e];
       }
     }
   }
@@ -316,7 +320,12 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int spli
     const int j = (c * kWave + lane) * 8;
     if (j < h) {
       float yy[8], d[8];
-      load_f32<8>(y + o + j, yy);
+      if constexpr (kKeepY) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) yy[e] = yk[c][e];
+      } else {
+        load_f32<8>(y + o + j, yy);
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) d[e] = rr * (dg[c][e] - yy[e] * rr * proj);
       store_f32<8>(dy + o + j, d);
