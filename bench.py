@@ -65,7 +65,8 @@ def side_pass_bytes(w, name):
     what each pass must read and write at least (norm statistics: read the
     rows; norm apply: read the rows, write Z and the token-contiguous copy of
     x_hat, or U and the token-contiguous copy of U_hat; cross-entropy reduce: read the softmax partials;
-    seed: read P and write G in place)."""
+    seed: read P and write G in place; operand scale: read and write the
+    token-contiguous x_hat, read the per-token coefficients)."""
     N, h, V, I = w.n_tokens, w.hidden, w.vocab, w.intermediate
     es = 2 if w.dtype == "bf16" else 4
     ldn = (N + 63) // 64 * 64
@@ -77,6 +78,7 @@ def side_pass_bytes(w, name):
         "mlp pre-norm apply": N * h * es + N * 4 + N * h * es + h * ldn * es,
         "cross-entropy reduce": 2 * slices * ldn * 4 + 3 * N * 4,
         "logit seed": 2 * V * ldn * es + slices * ldn * 4,
+        "operand scale (or seed, if out of range)": 2 * h * ldn * es + 2 * N * 4,
         "exit norm backward": 2 * N * h * 4 + N * h * es,
     }
     return table.get(name)

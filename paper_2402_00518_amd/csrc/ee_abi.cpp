@@ -54,6 +54,7 @@ struct Layout {
   size_t u = 0, uhat = 0, rx = 0, hg = 0, act = 0, y = 0, dz = 0, dy = 0, dhg = 0, dhu = 0,
          dgpg = 0, dgpu = 0;
   size_t mu = 0, gsp = 0, gsum = 0, dbp = 0;  // LayerNorm mean; bias: G row sums, bias partials
+  size_t coef = 0, fb = 0;                    // unshifted form: s_n exp(-LSE_n), range-check flag
   ee::SplitTail zs{0, 0, 1};                  // split-K tail of the dZ product
   ee::SplitTail ys{0, 0, 1};                  // split-K tail of the down projection
   int64_t gchunks = 0;
@@ -92,6 +93,8 @@ Layout layout(const ee_exit &e, int64_t n) {
   L.lse = take(ldn * 4);
   L.sn = take(ldn * 4);
   L.bsum = take(static_cast<size_t>(cdiv64(n, 32)) * 4);
+  L.coef = take(ldn * 4);
+  L.fb = take(4);
   if (normed) L.dgp = take(static_cast<size_t>(L.vtiles) * h * 4);
   if (e.norm == EE_NORM_LAYER) L.mu = take(ldn * 4);
   if (e.beta != nullptr) {
@@ -300,6 +303,8 @@ hipEvent_t prof_event() {
 char *at(void *ws, size_t off) { return static_cast<char *>(ws) + off; }
 float *atf(void *ws, size_t off) { return reinterpret_cast<float *>(at(ws, off)); }
 
+bool unshifted_form(const ee_exit &e) { return e.beta == nullptr && e.vocab >= 64; }
+
 // Forward of one exit; see ee_head_forward_loss.
 ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, const float *token_w, int64_t n64,
                       float w_e, uint32_t flags, void *ws, float *loss, float *row_loss, float *total, int first,
@@ -309,10 +314,17 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   const int n = static_cast<int>(n64), h = static_cast<int>(e.hidden), V = static_cast<int>(e.vocab);
   const int I = static_cast<int>(e.intermediate), ldn = static_cast<int>(L.ldn);
   const void *zsrc = x;
-  // The first exit of a call clears the device error record in its first kernel.
+  // The first exit of a call clears the device error record in its first
+  // kernel; every exit's first kernel clears its range-check flag.
   int *clear = first ? reinterpret_cast<int *>(at(ws, kFlagOff)) : nullptr;
+  // Exits without a bias take the unshifted form of the logits (P = exp(S));
+  // with a bias the seed also sums G's rows, so they keep the shifted form,
+  // and so does a vocabulary of less than one 64-id slice (where the seed
+  // costs nothing, and a single id keeps its loss exactly 0: exp(S - m) = 1).
+  const bool unshifted = unshifted_form(e);
+  int *fb = reinterpret_cast<int *>(at(ws, L.fb));
   if (e.kind == EE_EXIT_MLP) {
-    EE_LAUNCH("mlp pre-norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.rx), s, nullptr, clear));
+    EE_LAUNCH("mlp pre-norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.rx), s, nullptr, clear, fb));
     EE_LAUNCH("mlp pre-norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.rx), e.gamma_mlp, n, ldn, h, at(ws, L.u),
                                  nullptr, at(ws, L.uhat), s));
     EE_LAUNCH("gate and up projections + swiglu", s, ee::gemm_gate_up_swiglu(f32, at(ws, L.u), e.w_gate, e.w_up, n, I, h, at(ws, L.hg),
@@ -324,16 +336,16 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
     zsrc = at(ws, L.z);
   } else if (e.kind == EE_EXIT_NORM) {
     float *mu = e.norm == EE_NORM_LAYER ? atf(ws, L.mu) : nullptr;
-    EE_LAUNCH("exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s, mu, clear));
+    EE_LAUNCH("exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s, mu, clear, fb));
     EE_LAUNCH("exit norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.r), e.gamma, n, ldn, h, at(ws, L.z), nullptr,
                                  at(ws, L.zht), s, mu, e.beta));
     zsrc = at(ws, L.z);
   } else {
     EE_LAUNCH("hidden-state transpose", s, ee::launch_norm_apply(f32, f32, x, h, nullptr, nullptr, n, ldn, h, nullptr, nullptr, at(ws, L.zht), s,
-                                                                 nullptr, nullptr, clear));
+                                                                 nullptr, nullptr, clear, fb));
   }
   EE_LAUNCH("logits + softmax partials", s, ee::gemm_logits(f32, e.w_out, zsrc, V, n, h, at(ws, L.P), ldn, atf(ws, L.pm), atf(ws, L.pl),
-                         atf(ws, L.tgt), targets, s));
+                         atf(ws, L.tgt), targets, s, unshifted ? 1 : 0));
   ee::CeReduceArgs a{};
   a.part_m = atf(ws, L.pm);
   a.part_l = atf(ws, L.pl);
@@ -351,10 +363,27 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   a.tiles = static_cast<int>(L.vtiles);
   a.exit_weight = w_e;
   a.dynamic_weights = (flags & EE_FLAG_DYNAMIC_TOKEN_WEIGHTS) ? 1 : 0;
+  a.shift0 = unshifted ? 1 : 0;
+  a.fallback = fb;
+  a.coef = atf(ws, L.coef);
   EE_LAUNCH("cross-entropy reduce", s, ee::launch_ce_reduce(a, s));
   const bool bias = e.beta != nullptr;
-  EE_LAUNCH("logit seed", s, ee::launch_seed(f32, at(ws, L.P), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), targets, n, ldn, V, L.vtile, s,
-                                             bias ? atf(ws, L.gsp) : nullptr));
+  if (unshifted) {
+    // G = diag(coef) P' (see launch_seed_or_scale), unless a row was out of
+    // the unshifted range: then the launches gated on its flag redo the
+    // logits, the reduce and the seed in the shifted form.
+    EE_LAUNCH("logits, shifted (if out of range)", s, ee::gemm_logits(f32, e.w_out, zsrc, V, n, h, at(ws, L.P), ldn, atf(ws, L.pm),
+                                                                      atf(ws, L.pl), atf(ws, L.tgt), targets, s, 0, fb));
+    a.shift0 = 0;
+    a.run_if = fb;
+    EE_LAUNCH("cross-entropy reduce, shifted (if out of range)", s, ee::launch_ce_reduce(a, s));
+    EE_LAUNCH("operand scale (or seed, if out of range)", s,
+              ee::launch_seed_or_scale(f32, at(ws, L.P), at(ws, L.zht), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), atf(ws, L.coef),
+                                       targets, n, ldn, h, V, L.vtile, fb, s));
+  } else {
+    EE_LAUNCH("logit seed", s, ee::launch_seed(f32, at(ws, L.P), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), targets, n, ldn, V, L.vtile,
+                                               s, bias ? atf(ws, L.gsp) : nullptr));
+  }
   if (bias)
     EE_LAUNCH("logit-gradient row sums", s, ee::launch_gain_reduce(atf(ws, L.gsp), static_cast<int>(L.gchunks), nullptr, 0, V,
                                                                    atf(ws, L.gsum), 0, s));
@@ -378,9 +407,11 @@ ee_status run_backward(const ee_exit &e, int64_t n64, void *ws, const ee_exit_gr
   if (bias)
     EE_LAUNCH("exit bias gradient", s, ee::launch_gain_reduce(atf(ws, L.dbp), static_cast<int>(L.vtiles), nullptr, 0, h, g.d_beta, acc, s));
   if (e.kind != EE_EXIT_MLP) return EE_OK;
+  const bool unshifted = unshifted_form(e);  // as in run_forward: G = diag(coef) P' unless the flag is set
   EE_LAUNCH("dZ", s, ee::gemm_dz(f32, at(ws, L.P), e.w_out, n, ldn, h, V, atf(ws, L.dz), s, L.zs));
   EE_LAUNCH("exit norm backward", s, ee::launch_norm_bwd(f32, atf(ws, L.dz), atf(ws, L.y), atf(ws, L.r), e.gamma, n, h, at(ws, L.dy), s,
-                                                         L.zs));
+                                                         L.zs, unshifted ? atf(ws, L.coef) : nullptr,
+                                                         reinterpret_cast<const int *>(at(ws, L.fb))));
   EE_LAUNCH("dA + swiglu backward, down gradient", s,
             ee::gemm_da_swiglu_dw_down(f32, at(ws, L.dy), e.w_down, n, I, h, at(ws, L.hg), at(ws, L.dhg), at(ws, L.dhu),
                                        ldn, at(ws, L.act), g.d_w_down, acc, s));

@@ -151,9 +151,13 @@ template <typename T> using Raw4 = typename Raw4Of<T>::type;
 // m = max_v S and l = sum_v exp(S - m), stores P = exp(S - m) (the only copy
 // of the logits that reaches memory) at P[v][n], tokens contiguous, and
 // captures the fp32 logit of each token's target (next-token NLL, Sec. 2).
-// Rows are handled in parts of two blocks (32 slots), each reduced over the
-// wave's columns by a reduce-scatter (one row per lane) and broadcast back
-// through the wave's own LDS rows.  A part's 64 tokens are one 128-byte
+// With shift0 the store and the sums take no shift at all, P = exp(S) and
+// l = sum_v exp(S) (m is still the slice maximum, for the range check and
+// the confidence): the form in which the weight-gradient GEMM can use P
+// as it is (see the cross-entropy reduce).  Rows are handled in parts of two
+// blocks (32 slots), each reduced over the wave's columns by a
+// reduce-scatter (one row per lane) and, for the shifted form, broadcast
+// back through the wave's own LDS rows.  A part's 64 tokens are one 128-byte
 // line of a bf16 P row: in bf16 the part's P values pass through 8 KB of
 // the wave's LDS ([64 vocab ids][64 tokens], 16-byte chunks XOR-swizzled by
 // the vocab id) and leave in whole lines, eight lanes per line (a lane's own
@@ -169,6 +173,7 @@ struct EpiLogits {
     float *part_l;      // [V / WN][ldp]
     float *tgt;         // [ldp] target logit
     const int32_t *targets;
+    int shift0;         // P = exp(S) instead of exp(S - m)
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
@@ -202,8 +207,9 @@ struct EpiLogits {
     });
     const bool capture = __any(hit);
     const bool interior = t.m0 + Cfg::BM <= t.M && cbase + Cfg::WN <= t.N;
+    with_flag(p.shift0 != 0, [&](auto S0_) EE_ALWAYS_INLINE {
     with_flag(interior, [&](auto IN_) EE_ALWAYS_INLINE {
-      constexpr bool kIn = decltype(IN_)::value;
+      constexpr bool kIn = decltype(IN_)::value, kShift0 = decltype(S0_)::value;
       int col[NB];
       bool cok[NB];
       T *pcol[NB];  // P[col][m0 + rbase]: the group (I, Q) adds I*32 + Q*8
@@ -246,18 +252,22 @@ struct EpiLogits {
           });
         }
         slot_reduce_scatter<true>(mx, lane);
-        wl[slot_row(I0 * 16 + lo, lane)] = mx[0];
-        // the rows read back below are this wave's own: a wave-scope fence
-        // suffices (the other waves go on with their parts)
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        // P = exp(S - m) = exp2(S log2e - m log2e), four tokens per store; row sums
+        if constexpr (!kShift0) {
+          wl[slot_row(I0 * 16 + lo, lane)] = mx[0];
+          // the rows read back below are this wave's own: a wave-scope fence
+          // suffices (the other waves go on with their parts)
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        }
+        // P = exp(S - m) = exp2(S log2e - m log2e) (m = 0 with shift0), four
+        // tokens per store; row sums
         static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
           constexpr int I = I0 + decltype(ii)::value;
           static_for<4>([&](auto q) EE_ALWAYS_INLINE {
             constexpr int Q = decltype(q)::value;
-            const f32x4_t ml = *reinterpret_cast<const f32x4_t *>(wl + I * 32 + Q * 8 + hw * 4) * kLog2e;
+            const f32x4_t ml = kShift0 ? f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}
+                                       : *reinterpret_cast<const f32x4_t *>(wl + I * 32 + Q * 8 + hw * 4) * kLog2e;
             const bool rok = kIn || t.m0 + rbase + I * 32 + Q * 8 < t.M;
             f32x4_t s4 = {0.0f, 0.0f, 0.0f, 0.0f};
             static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
@@ -307,6 +317,7 @@ struct EpiLogits {
           p.part_l[ct * p.ldp + row] = sm[0];
         }
       });
+    });
     });
   }
 };

@@ -26,6 +26,8 @@
 // v_mfma_f32_32x32x2_f32; both accumulate in fp32.
 #pragma once
 
+#include <algorithm>
+
 #include "ee_device.h"
 
 namespace ee {
@@ -580,6 +582,24 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_kernel(Ope
   gemm_block<T, AK, BKM, Epi, Cfg>(A, B, s, ep, blockIdx.x, gridDim.x, blockIdx.z, smem);
 }
 
+// The same product for a launch that usually has nothing to do: it runs
+// only if *run_if is non-zero (a flag an earlier kernel of the stream set),
+// one block per CU looping over the tiles.  The grid is a multiple of the
+// XCD count, so tile t still runs on XCD t mod 8 and keeps its place in the
+// XCD-aware order; when the flag is clear the launch costs one round of
+// blocks that read it and return.
+template <typename T, bool AK, bool BKM, class Epi, class Cfg>
+__global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_gated_kernel(Operand A, Operand B, GemmShape s,
+                                                                      typename Epi::Params ep, const int *run_if) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * Cfg::STAGE_BYTES];
+  if (*run_if == 0) return;  // the same word for every thread
+  const int tiles = cdiv(s.M, Cfg::BM) * cdiv(s.N, Cfg::BN);
+  for (int t = blockIdx.x; t < tiles; t += gridDim.x) {
+    gemm_block<T, AK, BKM, Epi, Cfg>(A, B, s, ep, t, tiles, 0, smem);
+    __syncthreads();  // the next tile's first stage overwrites what the epilogue used
+  }
+}
+
 // Two independent problems in one grid: blocks [0, blocks1) take problem 1,
 // blocks [base2, gridDim.x) problem 2, where base2 = blocks1 rounded up to a
 // multiple of 8 (the blocks in between do nothing), so that both keep the
@@ -624,6 +644,20 @@ hipError_t launch_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Pa
   }
   hipLaunchKernelGGL((gemm_kernel<T, AK, BKM, Epi, Cfg>), dim3(static_cast<unsigned>(blocks), 1, splits),
                      dim3(Cfg::THREADS), 0, stream, A, B, s, ep);
+  return hipGetLastError();
+}
+
+constexpr int kGatedBlocks = 256;  // one block per CU of a 256-CU GPU (a multiple of kNumXcd)
+
+template <typename T, bool AK, bool BKM, class Epi, class Cfg>
+hipError_t launch_gemm_gated(Operand A, Operand B, GemmShape s, const typename Epi::Params &ep, const int *run_if,
+                             hipStream_t stream) {
+  const int64_t tiles = static_cast<int64_t>(cdiv(s.M, Cfg::BM)) * cdiv(s.N, Cfg::BN);
+  if (tiles <= 0) return hipSuccess;
+  if (s.kchunk != 0 || run_if == nullptr || !gemm_shape_ok<T, AK, BKM>(A, B, s)) return hipErrorInvalidValue;
+  const int64_t blocks = std::min<int64_t>(kGatedBlocks, (tiles + kNumXcd - 1) / kNumXcd * kNumXcd);
+  hipLaunchKernelGGL((gemm_gated_kernel<T, AK, BKM, Epi, Cfg>), dim3(static_cast<unsigned>(blocks)),
+                     dim3(Cfg::THREADS), 0, stream, A, B, s, ep, run_if);
   return hipGetLastError();
 }
 

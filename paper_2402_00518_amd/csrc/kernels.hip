@@ -77,10 +77,13 @@ template <int N> __device__ __forceinline__ void store_f32(bf16_t *p, const floa
 // pass over the row (no cancellation from subtracting squared means).
 template <typename Tin>
 __global__ __launch_bounds__(256) void row_rms_kernel(const Tin *x, int64_t ldx, int n, int h, float eps,
-                                                      float *r, float *mu, int *clear) {
+                                                      float *r, float *mu, int *clear, int *clear_exit) {
   constexpr int V = 16 / sizeof(Tin);
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (clear != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *clear = 0;  // a step's first kernel
+  if (blockIdx.x == 0 && threadIdx.x == 0) {  // a step's, or an exit's, first kernel
+    if (clear != nullptr) *clear = 0;
+    if (clear_exit != nullptr) *clear_exit = 0;
+  }
   if (row >= n) return;
   const Tin *xr = x + static_cast<int64_t>(row) * ldx;
   float mean = 0.0f;
@@ -216,9 +219,13 @@ __global__ __launch_bounds__(256) void row_norm_kernel(const Tin *x, int h, floa
 template <typename Tin, typename T>
 __global__ __launch_bounds__(256) void norm_apply_kernel(const Tin *x, int64_t ldx, const float *r,
                                                          const float *mu, const T *gain, const T *bias, int n,
-                                                         int ldn, int h, T *z, T *x_hat, T *x_hat_t, int *clear) {
+                                                         int ldn, int h, T *z, T *x_hat, T *x_hat_t, int *clear,
+                                                         int *clear_exit) {
   __shared__ float tile[64][65];
-  if (clear != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *clear = 0;  // a step's first kernel
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {  // a step's, or an exit's, first kernel
+    if (clear != nullptr) *clear = 0;
+    if (clear_exit != nullptr) *clear_exit = 0;
+  }
   const int n0 = blockIdx.x * 64, j0 = blockIdx.y * 64;
   const int tid = threadIdx.x;
   const int tr = tid >> 2, tc = (tid & 3) * 16;
@@ -284,7 +291,7 @@ __device__ __forceinline__ void load_dz8(const float *dz, int64_t o, int ns, int
 template <typename T, int CH>
 __global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int splits, int64_t zstride, int tok0,
                                                        int feat0, const float *y, const float *r, const T *gain, int n,
-                                                       int h, T *dy) {
+                                                       int h, T *dy, const float *row_scale, const int *scale_off) {
   // One wave per row; the row's dZ * gain stays in registers (CH 8-wide
   // chunks per lane, h <= CH * 512) between the projection and the output,
   // so dZ's slices are read once; up to CH = 12 (h <= 6144) the row of Y
@@ -294,6 +301,9 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int spli
   if (row >= n) return;
   const int64_t o = static_cast<int64_t>(row) * h;
   const float rr = r[row];
+  // dZ's row as G W_out: with the unshifted logits the product was of P' and
+  // G = diag(row_scale) P' (unless *scale_off is set)
+  const float zs = row_scale != nullptr && *scale_off == 0 ? row_scale[row] : 1.0f;
   const int f0 = row >= tok0 ? feat0 : h;  // features from f0 on are split
   float dg[CH][8];
   float yk[kKeepY ? CH : 1][8];
@@ -308,7 +318,7 @@ __global__ __launch_bounds__(256) void norm_bwd_kernel(const float *dz, int spli
       load_f32<8>(gain + j, g);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        dg[c][e] *= g[e];
+        dg[c][e] *= g[e] * zs;
         s += dg[c][e] * yy[e] * rr;
         if constexpr (kKeepY) yk[c][e] = yy[e];
       }
@@ -346,11 +356,22 @@ __device__ __forceinline__ void lse_merge(float &m, float &l, float m2, float l2
 // 32 tokens per block: 8 threads of 4 consecutive tokens (16-byte loads) x 64
 // groups of slices (slices g, g + 64, ... of group g, all loads in flight),
 // merged through LDS in group order, so the result does not depend on timing.
+// SHIFT0: the slices' sums are of exp(S) itself (EpiLogits with shift0), so
+// LSE = log sum_s l_s; m is still the row maximum.  Such a row passes the
+// range check if LSE <= kUnshiftedMaxLse and max >= kUnshiftedMinMax (P up to
+// e^50, and coef = s_n e^-LSE, the scale of the operand it multiplies, at
+// least about 1e-26 s_n: both far inside the bf16 exponent range); any row
+// that fails sets *fallback, and the launches gated on it redo the exit's
+// logits, reduce and seed in the shifted form.  coef[n] = s_n exp(-LSE_n).
 constexpr int kCeGroups = 64;
 constexpr int kCeSlicesPerThread = 8;  // up to kCeGroups * 8 slices in one round of loads
+constexpr float kUnshiftedMaxLse = 50.0f;
+constexpr float kUnshiftedMinMax = -60.0f;
 
+template <bool SHIFT0>
 __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
   __shared__ float sm_m[kCeGroups][32], sm_l[kCeGroups][32];
+  if (a.run_if != nullptr && *a.run_if == 0) return;  // a gated rerun with nothing to redo
   const int tt = threadIdx.x & 7, g = threadIdx.x >> 3;
   const int n0 = blockIdx.x * 32 + tt * 4;  // < ldn: partials are padded to ldn tokens
   // Each thread: max over its slices, then the sum of l exp(m - max) (one
@@ -372,10 +393,18 @@ __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
       for (int q = 0; q < kCeSlicesPerThread; ++q)
         if (t0 + q * kCeGroups < a.tiles) mx = fmaxf(mx, pm[q][e]);
       float sl = 0.0f;
+      if constexpr (SHIFT0) {
 #pragma unroll
-      for (int q = 0; q < kCeSlicesPerThread; ++q)
-        if (t0 + q * kCeGroups < a.tiles && pl[q][e] > 0.0f) sl += pl[q][e] * fast_exp(pm[q][e] - mx);
-      lse_merge(m[e], l[e], mx, sl);
+        for (int q = 0; q < kCeSlicesPerThread; ++q)
+          if (t0 + q * kCeGroups < a.tiles) sl += pl[q][e];
+        m[e] = fmaxf(m[e], mx);
+        l[e] += sl;
+      } else {
+#pragma unroll
+        for (int q = 0; q < kCeSlicesPerThread; ++q)
+          if (t0 + q * kCeGroups < a.tiles && pl[q][e] > 0.0f) sl += pl[q][e] * fast_exp(pm[q][e] - mx);
+        lse_merge(m[e], l[e], mx, sl);
+      }
     }
   }
 #pragma unroll
@@ -396,14 +425,18 @@ __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const float lq = sm_l[sub * 4 + q][tk];
-    if (lq > 0.0f) ll += lq * fast_exp(sm_m[sub * 4 + q][tk] - mm);
+    if constexpr (SHIFT0)
+      ll += lq;
+    else if (lq > 0.0f)
+      ll += lq * fast_exp(sm_m[sub * 4 + q][tk] - mm);
   }
 #pragma unroll
   for (int o = 8; o > 0; o >>= 1) ll += __shfl_xor(ll, o, 16);
   if (sub == 0) {
     float contrib = 0.0f;
     if (n < a.n) {
-      const float lse = mm + logf(ll);
+      const float lse = SHIFT0 ? logf(ll) : mm + logf(ll);
+      if (SHIFT0 && !(lse <= kUnshiftedMaxLse && mm >= kUnshiftedMinMax)) *a.fallback = 1;  // NaN fails too
       const int y = a.targets[n];
       const bool ok = y >= 0 && y < a.vocab;
       if (!ok) *a.flag = 1;
@@ -411,7 +444,9 @@ __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
       float w = a.token_w != nullptr ? a.token_w[n] : 1.0f;
       if (a.dynamic_weights) w *= expf(mm - lse);  // detached confidence = max probability
       a.lse[n] = lse;
-      a.sn[n] = a.exit_weight * w / static_cast<float>(a.n);
+      const float sn = a.exit_weight * w / static_cast<float>(a.n);
+      a.sn[n] = sn;
+      if (SHIFT0) a.coef[n] = sn * expf(-lse);
       if (a.row_loss != nullptr) a.row_loss[n] = nll;
       contrib = w * nll;
     }
@@ -431,14 +466,15 @@ __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
 // coefficients are recomputed only where a group of 16 rows starts a new
 // vocab tile (once per 64-row softmax slice).
 constexpr int kSeedRows = 128;
+// One block of the seed: vocab rows bx * kSeedRows .., tokens by * 2048 ..
 template <typename T>
-__global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, const float *lse,
-                                                   const float *sn, const int32_t *targets, int n,
-                                                   int ldn, int vocab, int vtile, float *gsum_part) {
+__device__ __forceinline__ void seed_block(int bx, int by, T *P, const float *part_m, const float *lse,
+                                           const float *sn, const int32_t *targets, int n, int ldn, int vocab,
+                                           int vtile, float *gsum_part) {
   __shared__ float red[kSeedRows][4];
-  const int c0 = blockIdx.y * 2048 + threadIdx.x * 8;
+  const int c0 = by * 2048 + threadIdx.x * 8;
   if (gsum_part == nullptr && c0 >= ldn) return;
-  const int vb = blockIdx.x * kSeedRows;
+  const int vb = bx * kSeedRows;
   float cf[8], s[8], lz[8];
   int yy[8];
   bool ok[8];
@@ -512,8 +548,15 @@ __global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, co
   __syncthreads();
   const int rows_all = min(kSeedRows, vocab - vb);
   if (static_cast<int>(threadIdx.x) < rows_all)
-    gsum_part[static_cast<int64_t>(blockIdx.y) * vocab + vb + threadIdx.x] =
+    gsum_part[static_cast<int64_t>(by) * vocab + vb + threadIdx.x] =
         ((red[threadIdx.x][0] + red[threadIdx.x][1]) + red[threadIdx.x][2]) + red[threadIdx.x][3];
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, const float *lse,
+                                                   const float *sn, const int32_t *targets, int n,
+                                                   int ldn, int vocab, int vtile, float *gsum_part) {
+  seed_block<T>(blockIdx.x, blockIdx.y, P, part_m, lse, sn, targets, n, ldn, vocab, vtile, gsum_part);
 }
 
 __global__ __launch_bounds__(256) void final_loss_kernel(const float *bs, int nb, int n, float *loss,
@@ -601,14 +644,14 @@ __global__ __launch_bounds__(256) void gain_reduce_kernel(const float *pa, int t
   } while (0)
 
 hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps, float *r,
-                          hipStream_t stream, float *mu, int *clear) {
+                          hipStream_t stream, float *mu, int *clear, int *clear_exit) {
   const dim3 grid(cdiv(n, 4));
   if (x_f32)
     hipLaunchKernelGGL(row_rms_kernel<float>, grid, dim3(256), 0, stream, static_cast<const float *>(x), ldx,
-                       n, h, eps, r, mu, clear);
+                       n, h, eps, r, mu, clear, clear_exit);
   else
     hipLaunchKernelGGL(row_rms_kernel<bf16_t>, grid, dim3(256), 0, stream, static_cast<const bf16_t *>(x),
-                       ldx, n, h, eps, r, mu, clear);
+                       ldx, n, h, eps, r, mu, clear, clear_exit);
   return hipGetLastError();
 }
 
@@ -653,25 +696,28 @@ hipError_t launch_row_norm(bool x_f32, bool f32, const void *x, int n, int h, fl
 
 hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, const float *r,
                              const void *gain, int n, int ldn, int h, void *z, void *x_hat, void *x_hat_t,
-                             hipStream_t stream, const float *mu, const void *bias, int *clear) {
+                             hipStream_t stream, const float *mu, const void *bias, int *clear, int *clear_exit) {
   const dim3 grid(cdiv(ldn, 64), h / 64);
   EE_DISPATCH(f32, {
     if (x_f32)
       hipLaunchKernelGGL((norm_apply_kernel<float, T>), grid, dim3(256), 0, stream,
                          static_cast<const float *>(x), ldx, r, mu, static_cast<const T *>(gain),
                          static_cast<const T *>(bias), n, ldn, h, static_cast<T *>(z), static_cast<T *>(x_hat),
-                         static_cast<T *>(x_hat_t), clear);
+                         static_cast<T *>(x_hat_t), clear, clear_exit);
     else
       hipLaunchKernelGGL((norm_apply_kernel<bf16_t, T>), grid, dim3(256), 0, stream,
                          static_cast<const bf16_t *>(x), ldx, r, mu, static_cast<const T *>(gain),
                          static_cast<const T *>(bias), n, ldn, h, static_cast<T *>(z), static_cast<T *>(x_hat),
-                         static_cast<T *>(x_hat_t), clear);
+                         static_cast<T *>(x_hat_t), clear, clear_exit);
   });
   return hipGetLastError();
 }
 
 hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream) {
-  hipLaunchKernelGGL(ce_reduce_kernel, dim3(cdiv(a.n, 32)), dim3(512), 0, stream, a);
+  if (a.shift0)
+    hipLaunchKernelGGL(ce_reduce_kernel<true>, dim3(cdiv(a.n, 32)), dim3(512), 0, stream, a);
+  else
+    hipLaunchKernelGGL(ce_reduce_kernel<false>, dim3(cdiv(a.n, 32)), dim3(512), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -683,6 +729,73 @@ hipError_t launch_seed(bool f32, void *P, const float *part_m, const float *lse,
   const dim3 grid(cdiv(vocab, kSeedRows), seed_chunks(ldn));
   EE_DISPATCH(f32, hipLaunchKernelGGL(seed_kernel<T>, grid, dim3(256), 0, stream, static_cast<T *>(P), part_m,
                                       lse, sn, targets, n, ldn, vocab, vtile, gsum_part));
+  return hipGetLastError();
+}
+
+// The unshifted form's counterpart of the seed: G = diag(coef) P' with
+// P' = P except at each token's target, P'[y_n][n] = P[y_n][n] - exp(LSE_n)
+// (then coef_n P' = s_n (p - 1) there), so instead of rewriting P the
+// per-token factor goes into the other operand of the weight gradient:
+// x_hat_t[j][n] *= coef_n (token columns n..ldn-1 stay zero).  One block:
+// tokens bx * 2048 .., feature rows by * 8 .. + 7, each thread 8 tokens of
+// the 8 rows (all loads first); a thread of the row bands by < 8 also fixes
+// the target of its token c0 + by (h >= 64), one each.
+template <typename T>
+__device__ __forceinline__ void scale_block(int bx, int by, T *x_hat_t, T *P, const float *coef, const float *lse,
+                                            const int32_t *targets, int n, int ldn, int vocab) {
+  const int c0 = bx * 2048 + threadIdx.x * 8;
+  if (c0 >= ldn) return;
+  float cf[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) cf[e] = c0 + e < n ? coef[c0 + e] : 0.0f;
+  float v[8][8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) load_f32<8>(x_hat_t + static_cast<int64_t>(by * 8 + r) * ldn + c0, v[r]);
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[r][e] *= cf[e];
+    store_f32<8>(x_hat_t + static_cast<int64_t>(by * 8 + r) * ldn + c0, v[r]);
+  }
+  const int c = c0 + by;
+  if (by < 8 && c < n) {
+    const int y = targets[c];
+    if (y >= 0 && y < vocab) {
+      T *q = P + static_cast<int64_t>(y) * ldn + c;
+      *q = from_f32<T>(to_f32(*q) - expf(lse[c]));
+    }
+  }
+}
+
+// After the unshifted reduce: the seed if *fallback is set (the shifted
+// form was redone), else the operand scale.  One grid for either job (a
+// block past the job's blocks does nothing).
+template <typename T>
+__global__ __launch_bounds__(256) void seed_or_scale_kernel(T *P, T *x_hat_t, const float *part_m, const float *lse,
+                                                            const float *sn, const float *coef,
+                                                            const int32_t *targets, int n, int ldn, int h, int vocab,
+                                                            int vtile, const int *fallback) {
+  const int b = blockIdx.x;
+  if (*fallback != 0) {
+    const int sx = cdiv(vocab, kSeedRows), sy = cdiv(ldn, 2048);  // seed_chunks(ldn)
+    if (b < sx * sy) seed_block<T>(b % sx, b / sx, P, part_m, lse, sn, targets, n, ldn, vocab, vtile, nullptr);
+  } else {
+    const int cx = cdiv(ldn, 2048), cy = h / 8;
+    if (b < cx * cy) scale_block<T>(b % cx, b / cx, x_hat_t, P, coef, lse, targets, n, ldn, vocab);
+  }
+}
+
+hipError_t launch_seed_or_scale(bool f32, void *P, void *x_hat_t, const float *part_m, const float *lse,
+                                const float *sn, const float *coef, const int32_t *targets, int n, int ldn, int h,
+                                int vocab, int vtile, const int *fallback, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  if (h % 8 != 0 || h < 64 || ldn % 8 != 0 || fallback == nullptr) return hipErrorInvalidValue;
+  const int64_t blocks = std::max<int64_t>(static_cast<int64_t>(cdiv(vocab, kSeedRows)) * seed_chunks(ldn),
+                                           static_cast<int64_t>(cdiv(ldn, 2048)) * (h / 8));
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  EE_DISPATCH(f32, hipLaunchKernelGGL(seed_or_scale_kernel<T>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                                      stream, static_cast<T *>(P), static_cast<T *>(x_hat_t), part_m, lse, sn, coef,
+                                      targets, n, ldn, h, vocab, vtile, fallback));
   return hipGetLastError();
 }
 
@@ -701,7 +814,9 @@ hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *par
 }
 
 hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const float *r, const void *gain, int n,
-                           int h, void *dy, hipStream_t stream, SplitTail sp) {
+                           int h, void *dy, hipStream_t stream, SplitTail sp, const float *row_scale,
+                           const int *scale_off) {
+  if (row_scale != nullptr && scale_off == nullptr) return hipErrorInvalidValue;
   if (h > kNormBwdMaxH) return hipErrorInvalidValue;
   const int splits = sp.splits > 1 ? sp.splits : 1;
   const int t0 = splits > 1 ? sp.tok0 : n, f0 = splits > 1 ? sp.feat0 : h;
@@ -712,13 +827,13 @@ hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const floa
     const T *g = static_cast<const T *>(gain);
     T *d = static_cast<T *>(dy);
     if (h <= 2048)
-      hipLaunchKernelGGL((norm_bwd_kernel<T, 4>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d);
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 4>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d, row_scale, scale_off);
     else if (h <= 4096)
-      hipLaunchKernelGGL((norm_bwd_kernel<T, 8>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d);
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 8>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d, row_scale, scale_off);
     else if (h <= 6144)
-      hipLaunchKernelGGL((norm_bwd_kernel<T, 12>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d);
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 12>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d, row_scale, scale_off);
     else
-      hipLaunchKernelGGL((norm_bwd_kernel<T, 16>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d);
+      hipLaunchKernelGGL((norm_bwd_kernel<T, 16>), grid, dim3(256), 0, stream, dz, splits, zs, t0, f0, y, r, g, n, h, d, row_scale, scale_off);
   });
   return hipGetLastError();
 }
@@ -747,11 +862,19 @@ hipError_t run_gemm_pair(Operand A1, Operand B1, GemmShape s1, const typename Ep
 int gemm_part_cols(bool f32) { return f32 ? CfgSmall::WN : CfgBig::WN; }
 
 hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, int n, int h, void *P, int ldn,
-                       float *part_m, float *part_l, float *tgt, const int32_t *targets, hipStream_t stream) {
+                       float *part_m, float *part_l, float *tgt, const int32_t *targets, hipStream_t stream,
+                       int shift0, const int *run_if) {
   EE_DISPATCH(f32, {
-    typename EpiLogits<T>::Params ep{static_cast<T *>(P), ldn, part_m, part_l, tgt, targets};
-    return run_gemm<T, true, true, EpiLogits<T>>(Operand{z, h}, Operand{w_out, h}, GemmShape{n, vocab, h}, ep,
-                                                    stream);
+    typename EpiLogits<T>::Params ep{static_cast<T *>(P), ldn, part_m, part_l, tgt, targets, shift0};
+    const Operand A{z, h}, B{w_out, h};
+    const GemmShape sh{n, vocab, h};
+    if (run_if != nullptr) {
+      if constexpr (std::is_same<T, bf16_t>::value)
+        return launch_gemm_gated<T, true, true, EpiLogits<T>, CfgBig>(A, B, sh, ep, run_if, stream);
+      else
+        return launch_gemm_gated<T, true, true, EpiLogits<T>, CfgSmall>(A, B, sh, ep, run_if, stream);
+    }
+    return run_gemm<T, true, true, EpiLogits<T>>(A, B, sh, ep, stream);
   });
   return hipSuccess;
 }

@@ -28,10 +28,12 @@ int gemm_part_cols(bool f32);
 // Row statistics of the exit norm.  RMSNorm (mu == NULL): r[n] =
 // (mean_j x[n][j]^2 + eps)^(-1/2).  LayerNorm: mu[n] = mean_j x[n][j] and
 // r[n] = (mean_j (x[n][j] - mu[n])^2 + eps)^(-1/2).
-// clear (optional): the device error flag, set to 0 by the launch (the
-// first kernel of a step clears it instead of a launch of its own).
+// clear, clear_exit (optional): the device error flag and an exit's
+// range-check flag, set to 0 by the launch (the first kernel of a step, or
+// of an exit, clears them instead of a launch of its own).
 hipError_t launch_row_rms(bool x_f32, const void *x, int64_t ldx, int n, int h, float eps,
-                          float *r, hipStream_t stream, float *mu = nullptr, int *clear = nullptr);
+                          float *r, hipStream_t stream, float *mu = nullptr, int *clear = nullptr,
+                          int *clear_exit = nullptr);
 // RMSNorm statistics of the fp32 rows the split down projection leaves
 // (see gemm_down_residual): the split outputs are first replaced by the sum
 // of their slices, in slice order.
@@ -41,11 +43,11 @@ hipError_t launch_row_rms_split(float *x, int n, int h, float eps, float *r, Spl
 // (mu == NULL: no centring; r == NULL: no scale), z = x_hat * gain + bias
 // (bias may be NULL).  Writes any of z [n][h], x_hat [n][h] (row-major) and
 // x_hat^T [h][ldn] (token-contiguous, columns n..ldn-1 zero).  Output
-// element type = `f32`.  clear: as for launch_row_rms.
+// element type = `f32`.  clear, clear_exit: as for launch_row_rms.
 hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, const float *r,
                              const void *gain, int n, int ldn, int h, void *z, void *x_hat,
                              void *x_hat_t, hipStream_t stream, const float *mu = nullptr,
-                             const void *bias = nullptr, int *clear = nullptr);
+                             const void *bias = nullptr, int *clear = nullptr, int *clear_exit = nullptr);
 
 // The exit norm of a few rows in one launch (decode): z[n][h] = (x - mu) r *
 // gain (+ bias), with mu the row mean when `centre` (LayerNorm), else 0, and
@@ -69,6 +71,10 @@ struct CeReduceArgs {
   int n, ldn, vocab, tiles;
   float exit_weight;
   int dynamic_weights;
+  int shift0;             // the partials are of exp(S) (EpiLogits shift0), see kernels.hip
+  int *fallback;          // shift0: set to 1 if a row is outside the unshifted range
+  float *coef;            // shift0: [ldn] s_n exp(-LSE_n)
+  const int *run_if;      // or NULL: run only if *run_if is non-zero
 };
 hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream);
 
@@ -80,6 +86,15 @@ hipError_t launch_seed(bool f32, void *P, const float *part_m, const float *lse,
                        const int32_t *targets, int n, int ldn, int vocab, int vtile, hipStream_t stream,
                        float *gsum_part = nullptr);
 
+// After the unshifted cross-entropy reduce: if *fallback is set, the seed
+// (as launch_seed, no row sums); else the operand scale, x_hat_t[j][c] *=
+// coef[c] (c < n) and, at each token's target, P[y_c][c] -= exp(lse[c]), so
+// that P holds P' with G = diag(coef) P'.  x_hat_t [h][ldn], P [V][ldn],
+// element type `f32`.
+hipError_t launch_seed_or_scale(bool f32, void *P, void *x_hat_t, const float *part_m, const float *lse,
+                                const float *sn, const float *coef, const int32_t *targets, int n, int ldn, int h,
+                                int vocab, int vtile, const int *fallback, hipStream_t stream);
+
 // loss[0] = sum(block_sums) / n;  total[0] = (first ? 0 : total[0]) + w * loss[0].
 hipError_t launch_final_loss(const float *block_sums, int blocks, int n, float *loss, float *total,
                              float w, int first, hipStream_t stream);
@@ -90,16 +105,21 @@ hipError_t launch_gain_reduce(const float *part_a, int tiles_a, const float *par
 
 // RMSNorm backward through the exit norm of an MLP exit:
 //   dz_hat = dZ * gain,  z_hat = y * r,  dY = r (dz_hat - z_hat mean_j(dz_hat z_hat)),
-// with dZ as gemm_dz leaves it for the split sp (its slices added in order).
+// with dZ as gemm_dz leaves it for the split sp (its slices added in order),
+// each row first scaled by row_scale[n] unless *scale_off is non-zero (dZ
+// computed from P', see launch_seed_or_scale).
 hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const float *r, const void *gain,
-                           int n, int h, void *dy, hipStream_t stream, SplitTail sp = SplitTail{0, 0, 1});
+                           int n, int h, void *dy, hipStream_t stream, SplitTail sp = SplitTail{0, 0, 1},
+                           const float *row_scale = nullptr, const int *scale_off = nullptr);
 
 
 // ------------------------------------------------------------------ GEMMs
-// Logits^T = W_out Z^T with the softmax-partials epilogue.
+// Logits^T = W_out Z^T with the softmax-partials epilogue (P = exp(S - m),
+// or exp(S) with shift0).  With run_if, a launch that runs only if *run_if
+// is non-zero (one block per CU looping over the tiles).
 hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, int n, int h, void *P,
                        int ldn, float *part_m, float *part_l, float *tgt, const int32_t *targets,
-                       hipStream_t stream);
+                       hipStream_t stream, int shift0 = 0, const int *run_if = nullptr);
 // dW[M][h] = (G^T X_hat) * gain with gain-gradient partials (K = tokens, both operands
 // token-contiguous with leading dimension ldn).  With a LayerNorm bias:
 // dW += gsum b^T and bias-gradient partials part_b (gsum[v] = sum_n G[n][v]).
@@ -134,6 +154,8 @@ hipError_t gemm_down_residual(bool f32, const void *act, const void *w_down, con
                               int h, int inter, float *y, hipStream_t stream, SplitTail sp = SplitTail{0, 0, 1});
 // dZ[n][h] = G W_out with G stored transposed [V][ldn]  (fp32 out), with
 // the split sp of its vocabulary sum (the buffer holds sp.splits n h floats).
+// (With the unshifted logits the operand is P' and G = diag(coef) P': the
+// norm backward applies coef, see launch_norm_bwd.)
 hipError_t gemm_dz(bool f32, const void *g_t, const void *w_out, int n, int ldn, int h, int vocab,
                    float *dz, hipStream_t stream, SplitTail sp = SplitTail{0, 0, 1});
 // One launch of two independent products of the MLP backward:

@@ -32,7 +32,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # per exit and step each; a tuple lists the alternatives, e.g. with and
 # without a split-K tail).
 LABEL_KERNELS = {
-    "logits + softmax partials": "ee::EpiLogits<",
+    "logits + softmax partials": "gemm_kernel<unsigned short, true, true, ee::EpiLogits<",
     "output-matrix gradient": "gemm_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
     "dZ": ("gemm_kernel<unsigned short, false, false, ee::EpiStoreF32<",
            "gemm_pair_kernel<unsigned short, false, false, ee::EpiStoreF32<"),
@@ -41,6 +41,7 @@ LABEL_KERNELS = {
     "down projection + residual": "ee::EpiResidual<",
     "dA + swiglu backward, down gradient": "ee::EpiSwiGLUBwd<",
     "logit seed": "seed_kernel",
+    "operand scale (or seed, if out of range)": "seed_or_scale_kernel",
     "cross-entropy reduce": "ce_reduce_kernel",
     # normalisation passes: statistics and apply of the exit norm (and of the
     # MLP pre-norm, whose input is the bf16 hidden state as well), the

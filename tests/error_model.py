@@ -29,7 +29,13 @@ and accumulation, fp32 weight gradients):
 The rounding points follow the precision convention of the boundary
 (norms, softmax and losses in fp32; GEMMs on bf16 operands with fp32
 accumulation; the logits stored once in bf16 as exp(S - m) and turned into
-the bf16 logit-gradient seed; weight gradients in fp32).  The result is a
+the bf16 logit-gradient seed G, or, for exits without a bias, stored as
+exp(S) with the per-token factor s_n exp(-LSE_n) rounded into the bf16
+token-contiguous x_hat and the target entries shifted by exp(LSE_n) in
+bf16; weight gradients in fp32).  Both forms round each term P x_hat of a
+weight gradient three times (P, then G or x_hat's scaled copy, and x_hat),
+so one variance covers both; the unshifted form's dZ = coef (P' W) rounds
+less and stays inside it.  The result is a
 standard deviation sigma per output element; the tests accept
 |gpu - oracle| <= K_SIGMA sigma + floor.  A single dominant term of a sum
 is covered as well: its error is at most a few u times the term, while
@@ -66,8 +72,15 @@ def acc_coef(k):
 
 
 def mm(a, b):
-    """Product of two variance-sized arrays in fp32 (a variance needs a few
-    significant digits, not fp64)."""
+    """Product of two variance-sized arrays.  A variance needs a few
+    significant digits, so the full-size products run in fp32; small ones
+    run in fp64, whose range also holds the squared rounding errors of
+    probabilities far below one (an fp32 variance of an element near 1e-22
+    underflows to zero)."""
+    a = np.asarray(a)
+    b = np.asarray(b)
+    if a.size * (b.shape[-1] if b.ndim > 1 else 1) <= 1 << 26:
+        return np.asarray(a, dtype=np.float64) @ np.asarray(b, dtype=np.float64)
     return (np.asarray(a, dtype=np.float32) @ np.asarray(b, dtype=np.float32)).astype(np.float64)
 
 

@@ -393,6 +393,63 @@ def test_mlp_gate_and_up_in_one_buffer():
     compare_full(s, b, case="gate_up_alias")
 
 
+# Exits without a bias keep the logits unshifted (P = exp(S)) when every
+# row's LSE is at most 50 and its largest logit at least -60; otherwise the
+# step redoes the exit's logits, reduce and seed in the shifted form.  These
+# cases force the second path: logits scaled up past the range (Norm, MLP,
+# Embedding exits, and a ragged shape), and rows whose logits all lie far
+# below zero.
+FALLBACK_CASES = [
+    ("range_large_norm", W.EXIT_NORM, 300, 256, 1000, 0, "bf16"),
+    ("range_large_norm_ragged", W.EXIT_NORM, 130, 192, 700, 0, "bf16"),
+    ("range_large_mlp", W.EXIT_MLP, 260, 192, 900, 320, "bf16"),
+    ("range_large_embedding", W.EXIT_EMBEDDING, 200, 128, 600, 0, "bf16"),
+    ("range_large_f32", W.EXIT_NORM, 150, 128, 300, 0, "f32"),
+]
+
+
+@pytest.mark.parametrize("name,kind,n,h,v,inter,dtype", FALLBACK_CASES, ids=[c[0] for c in FALLBACK_CASES])
+def test_logits_out_of_the_unshifted_range(name, kind, n, h, v, inter, dtype):
+    say(f"case: {name} (logits scaled past the unshifted range)")
+    b = small(kind, n, h, v, inter, dtype, seed=71, name=name)
+    ex = b.exits[0]
+    w = W.decode(ex.w_out)
+    # rows of Z have norm about sqrt(h) (Embedding: the raw hidden rows);
+    # aim the largest logits near 90
+    scale = 90.0 / (3.0 * 0.02 * math.sqrt(h) * (3.0 if kind == W.EXIT_EMBEDDING else 1.0))
+    ex.w_out = W._store((w * scale).astype(np.float32), dtype)
+    s = run(b)
+    _, per = compare_full(s, b, case=name,
+                          loss_rtol=LOSS_RTOL if dtype == "bf16" else 1e-5,
+                          grad_rtol=GRAD_RTOL if dtype == "bf16" else 1e-4)
+    lse_max = max(float(np.max(r.row_loss)) for r in per)
+    say(f"  {name}: largest row NLL {lse_max:.1f}")
+
+
+def test_logits_all_far_below_zero():
+    """Rows whose every logit is far below zero (their largest near -67):
+    under -60, so the step takes the shifted form."""
+    say("case: every logit near -80")
+    n, h, v = 200, 128, 700
+    b = small(W.EXIT_NORM, n, h, v, 0, "bf16", seed=73, name="range_negative", random_gamma=False)
+    ex = b.exits[0]
+    # hidden rows near a constant give x_hat near 1 and, with gamma = 1,
+    # logits near sum_j W[v][j] = -80 (-74 on average) with a spread of
+    # about 2 over the vocabulary, so that softmax rows and their roundings
+    # differ from token to token
+    rng = np.random.default_rng(5)
+    b.hidden[0] = W._store((0.5 + 0.2 * rng.standard_normal((n, h))).astype(np.float32), "bf16")
+    w = -80.0 / h + 0.2 * rng.standard_normal((v, h))
+    ex.w_out = W._store(w.astype(np.float32), "bf16")
+    x = W.decode(b.hidden[0])
+    z = x / np.sqrt((x * x).mean(1, keepdims=True) + 1e-5)
+    smax = (z @ W.decode(ex.w_out).T).max(1)
+    assert smax.max() < -60.0, smax.max()  # every row is out of the unshifted range
+    s = run(b)
+    total, _ = compare_full(s, b, case="range_negative")
+    assert math.isfinite(total)
+
+
 def test_out_of_range_target_is_reported():
     say("case: target outside the vocabulary")
     from paper_2402_00518_amd import binding as B
