@@ -345,7 +345,8 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
                                                                  nullptr, nullptr, clear, fb));
   }
   EE_LAUNCH("logits + softmax partials", s, ee::gemm_logits(f32, e.w_out, zsrc, V, n, h, at(ws, L.P), ldn, atf(ws, L.pm), atf(ws, L.pl),
-                         atf(ws, L.tgt), targets, s, unshifted ? 1 : 0));
+                         atf(ws, L.tgt), targets, s,
+                         unshifted ? ((flags & EE_FLAG_DYNAMIC_TOKEN_WEIGHTS) ? 1 : 2) : 0));
   ee::CeReduceArgs a{};
   a.part_m = atf(ws, L.pm);
   a.part_l = atf(ws, L.pl);

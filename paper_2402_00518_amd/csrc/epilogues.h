@@ -152,9 +152,10 @@ template <typename T> using Raw4 = typename Raw4Of<T>::type;
 // of the logits that reaches memory) at P[v][n], tokens contiguous, and
 // captures the fp32 logit of each token's target (next-token NLL, Sec. 2).
 // With shift0 the store and the sums take no shift at all, P = exp(S) and
-// l = sum_v exp(S) (m is still the slice maximum, for the range check and
-// the confidence): the form in which the weight-gradient GEMM can use P
-// as it is (see the cross-entropy reduce).  Rows are handled in parts of two
+// l = sum_v exp(S): the form in which the weight-gradient GEMM can use P as
+// it is (see the cross-entropy reduce); m, then needed only for the
+// confidence of dynamic token weights, is computed and stored only if
+// shift0 == 1 (2: no maxima at all).  Rows are handled in parts of two
 // blocks (32 slots), each reduced over the wave's columns by a
 // reduce-scatter (one row per lane) and, for the shifted form, broadcast
 // back through the wave's own LDS rows.  A part's 64 tokens are one 128-byte
@@ -173,7 +174,7 @@ struct EpiLogits {
     float *part_l;      // [V / WN][ldp]
     float *tgt;         // [ldp] target logit
     const int32_t *targets;
-    int shift0;         // P = exp(S) instead of exp(S - m)
+    int shift0;         // 1, 2: P = exp(S) instead of exp(S - m); 2: and no maxima
   };
   template <class Cfg>
   __device__ __forceinline__ static void apply(const Params &p, f32x16_t (&acc)[Cfg::MB][Cfg::NB], const TileCtx<Cfg> &t) {
@@ -207,9 +208,17 @@ struct EpiLogits {
     });
     const bool capture = __any(hit);
     const bool interior = t.m0 + Cfg::BM <= t.M && cbase + Cfg::WN <= t.N;
-    with_flag(p.shift0 != 0, [&](auto S0_) EE_ALWAYS_INLINE {
+    auto shift_modes = [&](auto &&f) EE_ALWAYS_INLINE {
+      if (p.shift0 == 0)
+        f(std::false_type{}, std::true_type{});
+      else if (p.shift0 == 1)
+        f(std::true_type{}, std::true_type{});
+      else
+        f(std::true_type{}, std::false_type{});
+    };
+    shift_modes([&](auto S0_, auto MX_) EE_ALWAYS_INLINE {
     with_flag(interior, [&](auto IN_) EE_ALWAYS_INLINE {
-      constexpr bool kIn = decltype(IN_)::value, kShift0 = decltype(S0_)::value;
+      constexpr bool kIn = decltype(IN_)::value, kShift0 = decltype(S0_)::value, kMax = decltype(MX_)::value;
       int col[NB];
       bool cok[NB];
       T *pcol[NB];  // P[col][m0 + rbase]: the group (I, Q) adds I*32 + Q*8
@@ -223,17 +232,19 @@ struct EpiLogits {
         // keep each part's accumulator reads inside the part (register pressure)
         __builtin_amdgcn_sched_barrier(0);
         float mx[32], sm[32];
-        static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
-          constexpr int I = I0 + decltype(ii)::value;
-          static_for<16>([&](auto v) EE_ALWAYS_INLINE {
-            constexpr int V = decltype(v)::value;
-            float m = -INFINITY;
-            static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
-              if (cok[j]) m = fmaxf(m, acc[I][j][V]);
+        if constexpr (kMax) {
+          static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
+            constexpr int I = I0 + decltype(ii)::value;
+            static_for<16>([&](auto v) EE_ALWAYS_INLINE {
+              constexpr int V = decltype(v)::value;
+              float m = -INFINITY;
+              static_for<NB>([&](auto j) EE_ALWAYS_INLINE {
+                if (cok[j]) m = fmaxf(m, acc[I][j][V]);
+              });
+              mx[decltype(ii)::value * 16 + V] = m;
             });
-            mx[decltype(ii)::value * 16 + V] = m;
           });
-        });
+        }
         if (capture) {
           static_for<2>([&](auto ii) EE_ALWAYS_INLINE {
             constexpr int I = I0 + decltype(ii)::value;
@@ -251,7 +262,7 @@ struct EpiLogits {
             });
           });
         }
-        slot_reduce_scatter<true>(mx, lane);
+        if constexpr (kMax) slot_reduce_scatter<true>(mx, lane);
         if constexpr (!kShift0) {
           wl[slot_row(I0 * 16 + lo, lane)] = mx[0];
           // the rows read back below are this wave's own: a wave-scope fence
@@ -313,7 +324,7 @@ struct EpiLogits {
         slot_reduce_scatter<false>(sm, lane);
         const int row = t.m0 + t.wave_m * Cfg::WM + slot_row(I0 * 16 + lo, lane);
         if (cbase < t.N && row < t.M) {
-          p.part_m[ct * p.ldp + row] = mx[0];
+          if constexpr (kMax) p.part_m[ct * p.ldp + row] = mx[0];
           p.part_l[ct * p.ldp + row] = sm[0];
         }
       });

@@ -357,16 +357,17 @@ __device__ __forceinline__ void lse_merge(float &m, float &l, float m2, float l2
 // groups of slices (slices g, g + 64, ... of group g, all loads in flight),
 // merged through LDS in group order, so the result does not depend on timing.
 // SHIFT0: the slices' sums are of exp(S) itself (EpiLogits with shift0), so
-// LSE = log sum_s l_s; m is still the row maximum.  Such a row passes the
-// range check if LSE <= kUnshiftedMaxLse and max >= kUnshiftedMinMax (P up to
-// e^50, and coef = s_n e^-LSE, the scale of the operand it multiplies, at
-// least about 1e-26 s_n: both far inside the bf16 exponent range); any row
-// that fails sets *fallback, and the launches gated on it redo the exit's
-// logits, reduce and seed in the shifted form.  coef[n] = s_n exp(-LSE_n).
+// LSE = log sum_s l_s (the maxima, read only for the confidence of dynamic
+// token weights, may be absent).  Such a row passes the range check if
+// |LSE| <= kUnshiftedLse: every logit is then at most 50 (P up to e^50) and
+// the largest at least -50 - ln V (> -64 for V <= 2^20, far from bf16's
+// e^-87), and coef = s_n e^-LSE, the scale of the operand it multiplies,
+// within s_n e^(+-50); any row that fails sets *fallback, and the launches
+// gated on it redo the exit's logits, reduce and seed in the shifted form.
+// coef[n] = s_n exp(-LSE_n).
 constexpr int kCeGroups = 64;
 constexpr int kCeSlicesPerThread = 8;  // up to kCeGroups * 8 slices in one round of loads
-constexpr float kUnshiftedMaxLse = 50.0f;
-constexpr float kUnshiftedMinMax = -60.0f;
+constexpr float kUnshiftedLse = 50.0f;
 
 template <bool SHIFT0>
 __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
@@ -377,13 +378,14 @@ __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
   // Each thread: max over its slices, then the sum of l exp(m - max) (one
   // exponential per slice, no chain of merges).
   float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, l[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  const bool with_max = !SHIFT0 || a.dynamic_weights;  // the unshifted form's maxima exist only for those
   for (int t0 = g; t0 < a.tiles; t0 += kCeGroups * kCeSlicesPerThread) {
     f32x4_t pm[kCeSlicesPerThread], pl[kCeSlicesPerThread];
 #pragma unroll
     for (int q = 0; q < kCeSlicesPerThread; ++q) {
       const int t = t0 + q * kCeGroups;
       const int64_t o = static_cast<int64_t>(min(t, a.tiles - 1)) * a.ldn + n0;
-      pm[q] = *reinterpret_cast<const f32x4_t *>(a.part_m + o);
+      pm[q] = with_max ? *reinterpret_cast<const f32x4_t *>(a.part_m + o) : f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
       pl[q] = *reinterpret_cast<const f32x4_t *>(a.part_l + o);
     }
 #pragma unroll
@@ -436,7 +438,7 @@ __global__ __launch_bounds__(512) void ce_reduce_kernel(CeReduceArgs a) {
     float contrib = 0.0f;
     if (n < a.n) {
       const float lse = SHIFT0 ? logf(ll) : mm + logf(ll);
-      if (SHIFT0 && !(lse <= kUnshiftedMaxLse && mm >= kUnshiftedMinMax)) *a.fallback = 1;  // NaN fails too
+      if (SHIFT0 && !(fabsf(lse) <= kUnshiftedLse)) *a.fallback = 1;  // NaN fails too
       const int y = a.targets[n];
       const bool ok = y >= 0 && y < a.vocab;
       if (!ok) *a.flag = 1;

@@ -71,7 +71,7 @@ struct CeReduceArgs {
   int n, ldn, vocab, tiles;
   float exit_weight;
   int dynamic_weights;
-  int shift0;             // the partials are of exp(S) (EpiLogits shift0), see kernels.hip
+  int shift0;             // the partials are of exp(S) (EpiLogits shift0 1 or 2), see kernels.hip
   int *fallback;          // shift0: set to 1 if a row is outside the unshifted range
   float *coef;            // shift0: [ldn] s_n exp(-LSE_n)
   const int *run_if;      // or NULL: run only if *run_if is non-zero
@@ -114,9 +114,10 @@ hipError_t launch_norm_bwd(bool f32, const float *dz, const float *y, const floa
 
 
 // ------------------------------------------------------------------ GEMMs
-// Logits^T = W_out Z^T with the softmax-partials epilogue (P = exp(S - m),
-// or exp(S) with shift0).  With run_if, a launch that runs only if *run_if
-// is non-zero (one block per CU looping over the tiles).
+// Logits^T = W_out Z^T with the softmax-partials epilogue: shift0 = 0,
+// P = exp(S - m); 1, P = exp(S) and the slice maxima; 2, P = exp(S) and no
+// maxima.  With run_if, a launch that runs only if *run_if is non-zero (one
+// block per CU looping over the tiles).
 hipError_t gemm_logits(bool f32, const void *w_out, const void *z, int vocab, int n, int h, void *P,
                        int ldn, float *part_m, float *part_l, float *tgt, const int32_t *targets,
                        hipStream_t stream, int shift0 = 0, const int *run_if = nullptr);
