@@ -78,7 +78,7 @@ def side_pass_bytes(w, name):
         "mlp pre-norm apply": N * h * es + N * 4 + N * h * es + h * ldn * es,
         "cross-entropy reduce": 2 * slices * ldn * 4 + 3 * N * 4,
         "logit seed": 2 * V * ldn * es + slices * ldn * 4,
-        "operand scale (or seed, if out of range)": 2 * h * ldn * es + 2 * N * 4,
+        "operand scale (or seed, if out of range) and loss": 2 * h * ldn * es + 2 * N * 4,
         "exit norm backward": 2 * N * h * 4 + N * h * es,
     }
     return table.get(name)

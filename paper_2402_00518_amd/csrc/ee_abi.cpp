@@ -378,9 +378,10 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
     a.shift0 = 0;
     a.run_if = fb;
     EE_LAUNCH("cross-entropy reduce, shifted (if out of range)", s, ee::launch_ce_reduce(a, s));
-    EE_LAUNCH("operand scale (or seed, if out of range)", s,
+    EE_LAUNCH("operand scale (or seed, if out of range) and loss", s,
               ee::launch_seed_or_scale(f32, at(ws, L.P), at(ws, L.zht), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), atf(ws, L.coef),
-                                       targets, n, ldn, h, V, L.vtile, fb, s));
+                                       targets, n, ldn, h, V, L.vtile, fb, atf(ws, L.bsum), static_cast<int>(cdiv64(n, 32)), loss,
+                                       total, w_e, first, s));
   } else {
     EE_LAUNCH("logit seed", s, ee::launch_seed(f32, at(ws, L.P), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), targets, n, ldn, V, L.vtile,
                                                s, bias ? atf(ws, L.gsp) : nullptr));
@@ -388,7 +389,8 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   if (bias)
     EE_LAUNCH("logit-gradient row sums", s, ee::launch_gain_reduce(atf(ws, L.gsp), static_cast<int>(L.gchunks), nullptr, 0, V,
                                                                    atf(ws, L.gsum), 0, s));
-  EE_LAUNCH("loss reduce", s, ee::launch_final_loss(atf(ws, L.bsum), static_cast<int>(cdiv64(n, 32)), n, loss, total, w_e, first, s));
+  if (!unshifted)
+    EE_LAUNCH("loss reduce", s, ee::launch_final_loss(atf(ws, L.bsum), static_cast<int>(cdiv64(n, 32)), n, loss, total, w_e, first, s));
   return EE_OK;
 }
 

@@ -561,8 +561,10 @@ __global__ __launch_bounds__(256) void seed_kernel(T *P, const float *part_m, co
   seed_block<T>(blockIdx.x, blockIdx.y, P, part_m, lse, sn, targets, n, ldn, vocab, vtile, gsum_part);
 }
 
-__global__ __launch_bounds__(256) void final_loss_kernel(const float *bs, int nb, int n, float *loss,
-                                                         float *total, float w, int first) {
+// The exit's loss from the reduce's block sums (fp64, fixed order); every
+// thread of a 256-thread block takes part.
+__device__ __forceinline__ void final_loss_block(const float *bs, int nb, int n, float *loss, float *total, float w,
+                                                 int first) {
   __shared__ double red[256];
   double s = 0.0;
   for (int i = threadIdx.x; i < nb; i += 256) s += bs[i];
@@ -577,6 +579,11 @@ __global__ __launch_bounds__(256) void final_loss_kernel(const float *bs, int nb
     loss[0] = L;
     if (total != nullptr) total[0] = (first ? 0.0f : total[0]) + w * L;
   }
+}
+
+__global__ __launch_bounds__(256) void final_loss_kernel(const float *bs, int nb, int n, float *loss,
+                                                         float *total, float w, int first) {
+  final_loss_block(bs, nb, n, loss, total, w, first);
 }
 
 // 32 columns x 8 groups of tiles per block; groups merge in a fixed order.
@@ -771,13 +778,25 @@ __device__ __forceinline__ void scale_block(int bx, int by, T *x_hat_t, T *P, co
 
 // After the unshifted reduce: the seed if *fallback is set (the shifted
 // form was redone), else the operand scale.  One grid for either job (a
-// block past the job's blocks does nothing).
+// block past the job's blocks does nothing); block 0 first turns the
+// reduce's block sums into the exit's loss (FinalLoss: as
+// launch_final_loss).
+struct FinalLoss {
+  const float *block_sums;
+  int blocks;
+  float *loss;
+  float *total;
+  float w;
+  int first;
+};
+
 template <typename T>
 __global__ __launch_bounds__(256) void seed_or_scale_kernel(T *P, T *x_hat_t, const float *part_m, const float *lse,
                                                             const float *sn, const float *coef,
                                                             const int32_t *targets, int n, int ldn, int h, int vocab,
-                                                            int vtile, const int *fallback) {
+                                                            int vtile, const int *fallback, FinalLoss fl) {
   const int b = blockIdx.x;
+  if (b == 0) final_loss_block(fl.block_sums, fl.blocks, n, fl.loss, fl.total, fl.w, fl.first);
   if (*fallback != 0) {
     const int sx = cdiv(vocab, kSeedRows), sy = cdiv(ldn, 2048);  // seed_chunks(ldn)
     if (b < sx * sy) seed_block<T>(b % sx, b / sx, P, part_m, lse, sn, targets, n, ldn, vocab, vtile, nullptr);
@@ -789,7 +808,8 @@ __global__ __launch_bounds__(256) void seed_or_scale_kernel(T *P, T *x_hat_t, co
 
 hipError_t launch_seed_or_scale(bool f32, void *P, void *x_hat_t, const float *part_m, const float *lse,
                                 const float *sn, const float *coef, const int32_t *targets, int n, int ldn, int h,
-                                int vocab, int vtile, const int *fallback, hipStream_t stream) {
+                                int vocab, int vtile, const int *fallback, const float *block_sums, int loss_blocks,
+                                float *loss, float *total, float w, int first, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
   if (h % 8 != 0 || h < 64 || ldn % 8 != 0 || fallback == nullptr) return hipErrorInvalidValue;
   const int64_t blocks = std::max<int64_t>(static_cast<int64_t>(cdiv(vocab, kSeedRows)) * seed_chunks(ldn),
@@ -797,7 +817,8 @@ hipError_t launch_seed_or_scale(bool f32, void *P, void *x_hat_t, const float *p
   if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
   EE_DISPATCH(f32, hipLaunchKernelGGL(seed_or_scale_kernel<T>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
                                       stream, static_cast<T *>(P), static_cast<T *>(x_hat_t), part_m, lse, sn, coef,
-                                      targets, n, ldn, h, vocab, vtile, fallback));
+                                      targets, n, ldn, h, vocab, vtile, fallback,
+                                      FinalLoss{block_sums, loss_blocks, loss, total, w, first}));
   return hipGetLastError();
 }
 

@@ -90,10 +90,12 @@ hipError_t launch_seed(bool f32, void *P, const float *part_m, const float *lse,
 // (as launch_seed, no row sums); else the operand scale, x_hat_t[j][c] *=
 // coef[c] (c < n) and, at each token's target, P[y_c][c] -= exp(lse[c]), so
 // that P holds P' with G = diag(coef) P'.  x_hat_t [h][ldn], P [V][ldn],
-// element type `f32`.
+// element type `f32`.  The same launch also does launch_final_loss's work
+// (block_sums .. first).
 hipError_t launch_seed_or_scale(bool f32, void *P, void *x_hat_t, const float *part_m, const float *lse,
                                 const float *sn, const float *coef, const int32_t *targets, int n, int ldn, int h,
-                                int vocab, int vtile, const int *fallback, hipStream_t stream);
+                                int vocab, int vtile, const int *fallback, const float *block_sums, int blocks,
+                                float *loss, float *total, float w, int first, hipStream_t stream);
 
 // loss[0] = sum(block_sums) / n;  total[0] = (first ? 0 : total[0]) + w * loss[0].
 hipError_t launch_final_loss(const float *block_sums, int blocks, int n, float *loss, float *total,

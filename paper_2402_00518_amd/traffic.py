@@ -41,7 +41,7 @@ LABEL_KERNELS = {
     "down projection + residual": "ee::EpiResidual<",
     "dA + swiglu backward, down gradient": "ee::EpiSwiGLUBwd<",
     "logit seed": "seed_kernel",
-    "operand scale (or seed, if out of range)": "seed_or_scale_kernel",
+    "operand scale (or seed, if out of range) and loss": "seed_or_scale_kernel",
     "cross-entropy reduce": "ce_reduce_kernel",
     # normalisation passes: statistics and apply of the exit norm (and of the
     # MLP pre-norm, whose input is the bf16 hidden state as well), the
