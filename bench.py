@@ -28,7 +28,8 @@ PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense MFMA
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # launch name -> label of the counter-measured traffic of the same kernel
-TRAFFIC_LABEL = {"exit norm rms": "norm statistics", "mlp pre-norm rms": "norm statistics",
+TRAFFIC_LABEL = {"exit norm": "norm (one pass)", "mlp pre-norm": "norm (one pass)",
+                 "exit norm rms": "norm statistics", "mlp pre-norm rms": "norm statistics",
                  "exit norm apply": "norm apply", "mlp pre-norm apply": "norm apply"}
 
 
@@ -62,9 +63,11 @@ def step_flops(w):
 
 def side_pass_bytes(w, name):
     """Algorithmic HBM bytes of one launch of the step's HBM-bound passes:
-    what each pass must read and write at least (norm statistics: read the
-    rows; norm apply: read the rows, write Z and the token-contiguous copy of
-    x_hat, or U and the token-contiguous copy of U_hat; cross-entropy reduce: read the softmax partials;
+    what each pass must read and write at least (the norm in one pass: read
+    the rows, write their scales, Z and the token-contiguous copy of x_hat, or
+    U and the token-contiguous copy of U_hat; norm statistics: read the rows;
+    norm apply: read the rows and the scales, write as the one pass does;
+    cross-entropy reduce: read the softmax partials;
     seed: read P and write G in place; operand scale: read and write the
     token-contiguous x_hat, read the per-token coefficients)."""
     N, h, V, I = w.n_tokens, w.hidden, w.vocab, w.intermediate
@@ -72,6 +75,8 @@ def side_pass_bytes(w, name):
     ldn = (N + 63) // 64 * 64
     slices = (V + 63) // 64
     table = {
+        "exit norm": N * h * es + N * 4 + N * h * es + h * ldn * es,
+        "mlp pre-norm": N * h * es + N * 4 + N * h * es + h * ldn * es,
         "exit norm rms": N * h * (4 if w.kind == 2 else es) + N * 4,
         "mlp pre-norm rms": N * h * es + N * 4,
         "exit norm apply": N * h * (4 if w.kind == 2 else es) + N * 4 + N * h * es + h * ldn * es,

@@ -324,9 +324,14 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   const bool unshifted = unshifted_form(e);
   int *fb = reinterpret_cast<int *>(at(ws, L.fb));
   if (e.kind == EE_EXIT_MLP) {
-    EE_LAUNCH("mlp pre-norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.rx), s, nullptr, clear, fb));
-    EE_LAUNCH("mlp pre-norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.rx), e.gamma_mlp, n, ldn, h, at(ws, L.u),
-                                 nullptr, at(ws, L.uhat), s));
+    if (ee::norm_rows(h, f32)) {
+      EE_LAUNCH("mlp pre-norm", s, ee::launch_norm_rows(f32, x, h, n, ldn, h, e.rms_eps, e.gamma_mlp, nullptr, atf(ws, L.rx),
+                                                        nullptr, at(ws, L.u), at(ws, L.uhat), s, clear, fb));
+    } else {
+      EE_LAUNCH("mlp pre-norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.rx), s, nullptr, clear, fb));
+      EE_LAUNCH("mlp pre-norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.rx), e.gamma_mlp, n, ldn, h,
+                                                               at(ws, L.u), nullptr, at(ws, L.uhat), s));
+    }
     EE_LAUNCH("gate and up projections + swiglu", s, ee::gemm_gate_up_swiglu(f32, at(ws, L.u), e.w_gate, e.w_up, n, I, h, at(ws, L.hg),
                                                                              at(ws, L.act), s));
     EE_LAUNCH("down projection + residual", s, ee::gemm_down_residual(f32, at(ws, L.act), e.w_down, x, n, h, I, atf(ws, L.y), s, L.ys));
@@ -336,9 +341,14 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
     zsrc = at(ws, L.z);
   } else if (e.kind == EE_EXIT_NORM) {
     float *mu = e.norm == EE_NORM_LAYER ? atf(ws, L.mu) : nullptr;
-    EE_LAUNCH("exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s, mu, clear, fb));
-    EE_LAUNCH("exit norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.r), e.gamma, n, ldn, h, at(ws, L.z), nullptr,
-                                 at(ws, L.zht), s, mu, e.beta));
+    if (ee::norm_rows(h, f32)) {
+      EE_LAUNCH("exit norm", s, ee::launch_norm_rows(f32, x, h, n, ldn, h, e.rms_eps, e.gamma, e.beta, atf(ws, L.r), mu,
+                                                     at(ws, L.z), at(ws, L.zht), s, clear, fb));
+    } else {
+      EE_LAUNCH("exit norm rms", s, ee::launch_row_rms(f32, x, h, n, h, e.rms_eps, atf(ws, L.r), s, mu, clear, fb));
+      EE_LAUNCH("exit norm apply", s, ee::launch_norm_apply(f32, f32, x, h, atf(ws, L.r), e.gamma, n, ldn, h, at(ws, L.z),
+                                                            nullptr, at(ws, L.zht), s, mu, e.beta));
+    }
     zsrc = at(ws, L.z);
   } else {
     EE_LAUNCH("hidden-state transpose", s, ee::launch_norm_apply(f32, f32, x, h, nullptr, nullptr, n, ldn, h, nullptr, nullptr, at(ws, L.zht), s,

@@ -273,6 +273,168 @@ __global__ __launch_bounds__(256) void norm_apply_kernel(const Tin *x, int64_t l
   store_f32<16>(x_hat_t + static_cast<int64_t>(j0 + fr) * ldn + n0 + tk, o);
 }
 
+// Norm of the exit (or the MLP pre-norm) in one pass: the 8 rows of a
+// block (one a wave) stay in LDS between their statistics and the two
+// outputs, so x is read once instead of twice (row_rms_kernel, then
+// norm_apply_kernel).  The per-lane order of the sums, the formulas and the
+// roundings are those two kernels', so r, mu, z and x_hat_t come out the
+// same.  Blocks of one XCD take consecutive row groups (the hardware gives
+// block b to XCD b mod 8), so the 8-token pieces of each line of x_hat_t are
+// written into one L2.  With rows of up to 8 KB two blocks share a CU (16
+// rows were slower: one block a CU, no overlap of its load and store
+// phases).
+template <typename Tin> __device__ __forceinline__ void unpack16(const u32x4_t &w, float (&v)[16 / sizeof(Tin)]) {
+  if constexpr (std::is_same<Tin, float>::value) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(w[e]);
+  } else {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      v[2 * d] = __uint_as_float(w[d] << 16);
+      v[2 * d + 1] = __uint_as_float(w[d] & 0xFFFF0000u);
+    }
+  }
+}
+
+constexpr int kNormRows = 8;              // rows of a block, one a wave
+constexpr int kNormRowsLds = 128 * 1024;  // at most, for the 8 rows of x
+
+template <typename Tin, typename T>
+__global__ __launch_bounds__(512) void norm_rows_kernel(const Tin *x, int64_t ldx, int n, int ldn, int h, float eps,
+                                                        const T *gain, const T *bias, float *r, float *mu, T *z,
+                                                        T *x_hat_t, int *clear, int *clear_exit) {
+  constexpr int R = kNormRows;
+  extern __shared__ __attribute__((aligned(16))) char rows_lds[];
+  __shared__ float row_r[R], row_m[R];
+  constexpr int V = 16 / sizeof(Tin);                // inputs per 16-byte chunk
+  constexpr int CH = kNormRowsLds / R / 16 / kWave;  // chunks of a row per lane, at most
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (blockIdx.x == 0 && tid == 0) {  // a step's, or an exit's, first kernel
+    if (clear != nullptr) *clear = 0;
+    if (clear_exit != nullptr) *clear_exit = 0;
+  }
+  const int groups = ldn / R, per = groups / kNumXcd, rem = groups % kNumXcd;
+  const int xcd = blockIdx.x % kNumXcd, idx = blockIdx.x / kNumXcd;
+  const int t0 = (xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx) * R;
+  Tin *lds = reinterpret_cast<Tin *>(rows_lds);
+
+  // Statistics of row t0 + wave: every load of the row first, then it goes
+  // to LDS and into the sums in row_rms_kernel's order.
+  const int row = t0 + wave;
+  float mean = 0.0f, rs = 0.0f;
+  if (row < n) {
+    const Tin *xr = x + static_cast<int64_t>(row) * ldx;
+    Tin *lr = lds + wave * h;
+    u32x4_t w[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int j = (lane + c * kWave) * V;
+      if (j < h) w[c] = *reinterpret_cast<const u32x4_t *>(xr + j);
+    }
+    float t = 0.0f, s = 0.0f;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int j = (lane + c * kWave) * V;
+      if (j < h) {
+        *reinterpret_cast<u32x4_t *>(lr + j) = w[c];
+        float v[V];
+        unpack16<Tin>(w[c], v);
+        if (mu != nullptr) {
+#pragma unroll
+          for (int e = 0; e < V; ++e) t += v[e];
+        } else {
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const float d = v[e] - mean;
+            s += d * d;
+          }
+        }
+      }
+    }
+    if (mu != nullptr) {  // LayerNorm: centred second pass, from LDS
+      mean = warp_sum(t) / static_cast<float>(h);
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        const int j = (lane + c * kWave) * V;
+        if (j < h) {
+          float v[V];
+          unpack16<Tin>(*reinterpret_cast<const u32x4_t *>(lr + j), v);
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const float d = v[e] - mean;
+            s += d * d;
+          }
+        }
+      }
+    }
+    s = warp_sum(s);
+    rs = 1.0f / sqrtf(s / static_cast<float>(h) + eps);
+    if (lane == 0) {
+      r[row] = rs;
+      if (mu != nullptr) mu[row] = mean;
+    }
+  }
+  if (lane == 0) {
+    row_r[wave] = rs;
+    row_m[wave] = mean;
+  }
+  __syncthreads();
+
+  // z, row-major: a thread takes 8 features (gain and bias loaded once) in
+  // every row, so each store of a wave is 1 KB of one row.
+  for (int j = tid * 8; j < h; j += 512 * 8) {
+    float g[8], b[8];
+    load_f32<8>(gain + j, g);
+    if (bias != nullptr) load_f32<8>(bias + j, b);
+#pragma unroll
+    for (int q = 0; q < R; ++q) {
+      if (t0 + q >= n) break;
+      float v[8], zz[8];
+      load_f32<8>(lds + q * h + j, v);
+      const float rq = row_r[q], m = row_m[q];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (v[e] - m) * rq;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) zz[e] = v[e] * g[e];
+      if (bias != nullptr) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) zz[e] += b[e];
+      }
+      store_f32<8>(z + static_cast<int64_t>(t0 + q) * h + j, zz);
+    }
+  }
+
+  // x_hat_t, token-contiguous: two features a thread, the block's 8 tokens
+  // each (zero past the last token, up to ldn).
+  float rr[R], mm[R];
+#pragma unroll
+  for (int q = 0; q < R; ++q) {
+    rr[q] = row_r[q];
+    mm[q] = row_m[q];
+  }
+  for (int j = 2 * tid; j < h; j += 1024) {
+    float o0[R], o1[R];
+#pragma unroll
+    for (int q = 0; q < R; ++q) {
+      float a, b;
+      if constexpr (std::is_same<Tin, float>::value) {
+        const u32x2_t p = *reinterpret_cast<const u32x2_t *>(lds + q * h + j);
+        a = __uint_as_float(p[0]);
+        b = __uint_as_float(p[1]);
+      } else {
+        const uint32_t p = *reinterpret_cast<const uint32_t *>(lds + q * h + j);
+        a = __uint_as_float(p << 16);
+        b = __uint_as_float(p & 0xFFFF0000u);
+      }
+      const bool ok = t0 + q < n;
+      o0[q] = ok ? (a - mm[q]) * rr[q] : 0.0f;
+      o1[q] = ok ? (b - mm[q]) * rr[q] : 0.0f;
+    }
+    store_f32<R>(x_hat_t + static_cast<int64_t>(j) * ldn + t0, o0);
+    store_f32<R>(x_hat_t + static_cast<int64_t>(j + 1) * ldn + t0, o1);
+  }
+}
+
 // RMSNorm backward, one wave per row (see launch.h for the formula).
 constexpr int kNormBwdMaxH = 16 * kWave * 8;  // 8192: at most 16 8-wide chunks per lane
 
@@ -720,6 +882,29 @@ hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, c
                          static_cast<T *>(x_hat_t), clear, clear_exit);
   });
   return hipGetLastError();
+}
+
+bool norm_rows(int h, bool x_f32) { return kNormRows * h * (x_f32 ? 4 : 2) <= kNormRowsLds; }
+
+hipError_t launch_norm_rows(bool f32, const void *x, int64_t ldx, int n, int ldn, int h, float eps, const void *gain,
+                            const void *bias, float *r, float *mu, void *z, void *x_hat_t, hipStream_t stream,
+                            int *clear, int *clear_exit) {
+  if (!norm_rows(h, f32) || h % 64 != 0 || ldn % 64 != 0 || n > ldn || gain == nullptr || z == nullptr ||
+      x_hat_t == nullptr)
+    return hipErrorInvalidValue;
+  const int lds = kNormRows * h * (f32 ? 4 : 2);
+  hipError_t e = hipSuccess;
+  EE_DISPATCH(f32, {
+    const auto k = norm_rows_kernel<T, T>;
+    e = hipFuncSetAttribute(reinterpret_cast<const void *>(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(k, dim3(ldn / kNormRows), dim3(512), lds, stream, static_cast<const T *>(x), ldx, n, ldn, h,
+                         eps, static_cast<const T *>(gain), static_cast<const T *>(bias), r, mu, static_cast<T *>(z),
+                         static_cast<T *>(x_hat_t), clear, clear_exit);
+      e = hipGetLastError();
+    }
+  });
+  return e;
 }
 
 hipError_t launch_ce_reduce(const CeReduceArgs &a, hipStream_t stream) {

@@ -49,6 +49,15 @@ hipError_t launch_norm_apply(bool x_f32, bool f32, const void *x, int64_t ldx, c
                              void *x_hat_t, hipStream_t stream, const float *mu = nullptr,
                              const void *bias = nullptr, int *clear = nullptr, int *clear_exit = nullptr);
 
+// launch_row_rms followed by launch_norm_apply (z and x_hat^T, a gain, an
+// optional bias) as one pass over x, for rows that fit a block's LDS
+// (norm_rows(h, f32): 8 rows of h inputs in at most 128 KB).  Same results;
+// x and the outputs are of the exit's element type `f32`.
+bool norm_rows(int h, bool f32);
+hipError_t launch_norm_rows(bool f32, const void *x, int64_t ldx, int n, int ldn, int h, float eps, const void *gain,
+                            const void *bias, float *r, float *mu, void *z, void *x_hat_t, hipStream_t stream,
+                            int *clear = nullptr, int *clear_exit = nullptr);
+
 // The exit norm of a few rows in one launch (decode): z[n][h] = (x - mu) r *
 // gain (+ bias), with mu the row mean when `centre` (LayerNorm), else 0, and
 // r = (mean (x - mu)^2 + eps)^(-1/2).  x is fp32 when x_f32, z is `f32`.

@@ -43,11 +43,13 @@ LABEL_KERNELS = {
     "logit seed": "seed_kernel",
     "operand scale (or seed, if out of range) and loss": "seed_or_scale_kernel",
     "cross-entropy reduce": "ce_reduce_kernel",
-    # normalisation passes: statistics and apply of the exit norm (and of the
-    # MLP pre-norm, whose input is the bf16 hidden state as well), the
-    # statistics that first add the split down projection's slices, the
-    # apply of the MLP exit norm to the fp32 residual stream, and the norm
-    # backward of the MLP exit
+    # normalisation passes: the exit norm (and the MLP pre-norm, whose input
+    # is the bf16 hidden state as well) in one pass, or as statistics and
+    # apply where a block's rows do not fit its LDS; the statistics that
+    # first add the split down projection's slices, the apply of the MLP
+    # exit norm to the fp32 residual stream, and the norm backward of the
+    # MLP exit
+    "norm (one pass)": "norm_rows_kernel<",
     "norm statistics": "row_rms_kernel<",
     "norm statistics (split sum)": "row_rms_split_kernel<",
     "norm apply": "norm_apply_kernel<unsigned short, unsigned short>",
