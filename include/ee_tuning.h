@@ -46,6 +46,10 @@ extern "C" {
 
 #define EE_ABI_VERSION 2
 
+/* Each enum below also spans every int value (the *_RANGE_* enumerators are
+ * never passed or returned): a caller may hand the library any int in one of
+ * these types, an unknown value is rejected with an error, and reading it is
+ * defined behaviour in the C++ library as well. */
 typedef enum ee_status {
   EE_OK = 0,
   EE_ERR_NULL = 1,        /* a required pointer is NULL                       */
@@ -56,10 +60,17 @@ typedef enum ee_status {
   EE_ERR_ALIAS = 6,       /* an output overlaps another output or an input    */
   EE_ERR_UNSUPPORTED = 7, /* exit kind or flag not implemented (Layer exit)   */
   EE_ERR_TARGET = 8,      /* device saw a target outside [0, V)               */
-  EE_ERR_HIP = 9          /* a HIP runtime call or launch failed              */
+  EE_ERR_HIP = 9,         /* a HIP runtime call or launch failed              */
+  EE_STATUS_RANGE_MIN = -0x7FFFFFFF - 1,
+  EE_STATUS_RANGE_MAX = 0x7FFFFFFF
 } ee_status;
 
-typedef enum ee_dtype { EE_F32 = 0, EE_BF16 = 1 } ee_dtype;
+typedef enum ee_dtype {
+  EE_F32 = 0,
+  EE_BF16 = 1,
+  EE_DTYPE_RANGE_MIN = -0x7FFFFFFF - 1,
+  EE_DTYPE_RANGE_MAX = 0x7FFFFFFF
+} ee_dtype;
 
 /* Exit architectures of Sec. 2.1 ("Architectures of early exits"):
  *  EMBEDDING  logits = X W_out^T                                  (one matrix)
@@ -73,7 +84,9 @@ typedef enum ee_exit_kind {
   EE_EXIT_EMBEDDING = 0,
   EE_EXIT_NORM = 1,
   EE_EXIT_MLP = 2,
-  EE_EXIT_LAYER = 3
+  EE_EXIT_LAYER = 3,
+  EE_EXIT_KIND_RANGE_MIN = -0x7FFFFFFF - 1,
+  EE_EXIT_KIND_RANGE_MAX = 0x7FFFFFFF
 } ee_exit_kind;
 
 /* Normalisation of a Norm exit (Sec. 2.1: "a LayerNorm or RMSNorm module").
@@ -81,7 +94,12 @@ typedef enum ee_exit_kind {
  *  LAYER  s_hat = (s - mean_j s_j) (mean_j (s_j - mean)^2 + eps)^(-1/2),
  *         z = s_hat * gamma + beta, with beta optional (NULL: no bias).
  * LAYER is available for NORM exits; MLP exits use RMSNorm. */
-typedef enum ee_norm { EE_NORM_RMS = 0, EE_NORM_LAYER = 1 } ee_norm;
+typedef enum ee_norm {
+  EE_NORM_RMS = 0,
+  EE_NORM_LAYER = 1,
+  EE_NORM_RANGE_MIN = -0x7FFFFFFF - 1,
+  EE_NORM_RANGE_MAX = 0x7FFFFFFF
+} ee_norm;
 
 /* Step flags. */
 #define EE_FLAG_DYNAMIC_TOKEN_WEIGHTS 1u

@@ -628,6 +628,7 @@ const char *ee_status_string(ee_status s) {
     case EE_ERR_UNSUPPORTED: return "unsupported exit kind or flag";
     case EE_ERR_TARGET: return "a target token id is outside [0, V)";
     case EE_ERR_HIP: return "HIP runtime error";
+    default: break;
   }
   return "unknown status";
 }
