@@ -354,6 +354,7 @@ struct EpiLogits {
 // block's W loads have been consumed, so no store waits on a load.
 template <typename T>
 struct EpiWeightGrad {
+  static constexpr bool kPersistent = true;  // launch_gemm runs it as one block per CU looping over the tiles
   struct Params {
     float *dW;          // [N][ldw]
     int64_t ldw;

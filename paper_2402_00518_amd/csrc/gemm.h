@@ -46,6 +46,7 @@ struct GemmShape {
 constexpr int kRowBytes = 128;
 constexpr int kNumXcd = 8;
 constexpr int kGroupM = 4;
+constexpr int kLoopBlocks = 256;  // grid of the looping kernels: one block per CU of a 256-CU GPU (a multiple of kNumXcd)
 
 template <int BM_, int BN_, int WM_, int WN_, int MIN_BLOCKS_>
 struct TileCfg {
@@ -178,6 +179,10 @@ struct KMajorPairLoader {
 // kPairB = true.
 template <class E, class = void> struct EpiPairB : std::false_type {};
 template <class E> struct EpiPairB<E, std::void_t<decltype(E::kPairB)>> : std::bool_constant<E::kPairB> {};
+// Epilogues whose GEMMs run as one block per CU looping over the tiles.
+template <class E, class = void> struct EpiPersistent : std::false_type {};
+template <class E>
+struct EpiPersistent<E, std::void_t<decltype(E::kPersistent)>> : std::bool_constant<E::kPersistent> {};
 
 // MN-major tile: BK k-rows x ROWS contiguous operand rows, written
 // transposed (k contiguous) into LDS.
@@ -459,13 +464,18 @@ __device__ __forceinline__ void tile_of_block(int b, int nblk, int tiles_m, int 
 
 // ----------------------------------------------------------------- kernel
 // Block b of nblk (b mod 8 = the XCD it runs on) of one GEMM problem, split-K
-// slice kz: main loop and epilogue of its tile.
-template <typename T, bool AK, bool BKM, class Epi, class Cfg>
+// slice kz: main loop and epilogue of its tile.  LOOP: the caller loops over
+// tiles; the thread index is then opaque to the compiler, so that no address
+// it derives is hoisted out of the loop and kept live through the epilogue
+// (which spilled registers).
+template <typename T, bool AK, bool BKM, class Epi, class Cfg, bool LOOP = false>
 __device__ __forceinline__ void gemm_block(const Operand &A, const Operand &B, const GemmShape &s,
                                            const typename Epi::Params &ep, int b, int nblk, int kz, char *smem) {
   constexpr int BK = 8 * Elem<T>::CH;
   constexpr int MB = Cfg::MB, NB = Cfg::NB;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int tid_v = threadIdx.x;
+  if constexpr (LOOP) asm volatile("" : "+v"(tid_v));
+  const int tid = tid_v, lane = tid & 63, wave = tid >> 6;
   const int wave_m = wave / Cfg::WAVES_N, wave_n = wave % Cfg::WAVES_N;
   const int tiles_m = cdiv(s.M, Cfg::BM), tiles_n = cdiv(s.N, Cfg::BN);
   int tile_m, tile_n;
@@ -595,7 +605,25 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_gated_kern
   if (*run_if == 0) return;  // the same word for every thread
   const int tiles = cdiv(s.M, Cfg::BM) * cdiv(s.N, Cfg::BN);
   for (int t = blockIdx.x; t < tiles; t += gridDim.x) {
-    gemm_block<T, AK, BKM, Epi, Cfg>(A, B, s, ep, t, tiles, 0, smem);
+    gemm_block<T, AK, BKM, Epi, Cfg, true>(A, B, s, ep, t, tiles, 0, smem);
+    __syncthreads();  // the next tile's first stage overwrites what the epilogue used
+  }
+}
+
+// One block per CU looping over the tiles, tile t on block t mod gridDim.x
+// (a multiple of 8, so on XCD t mod 8 as in the one-block-per-tile launch):
+// a CU starts its next tile's loads right after the epilogue's barrier,
+// without waiting for a new block to be dispatched (measured at 2.6 us
+// between one weight-gradient tile's end and the next one's start on the
+// freed CU).
+template <typename T, bool AK, bool BKM, class Epi, class Cfg>
+__global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_persistent_kernel(Operand A, Operand B,
+                                                                           GemmShape s,
+                                                                           typename Epi::Params ep) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * Cfg::STAGE_BYTES];
+  const int tiles = cdiv(s.M, Cfg::BM) * cdiv(s.N, Cfg::BN);
+  for (int t = blockIdx.x; t < tiles; t += gridDim.x) {
+    gemm_block<T, AK, BKM, Epi, Cfg, true>(A, B, s, ep, t, tiles, 0, smem);
     __syncthreads();  // the next tile's first stage overwrites what the epilogue used
   }
 }
@@ -642,12 +670,19 @@ hipError_t launch_gemm(Operand A, Operand B, GemmShape s, const typename Epi::Pa
     if (s.kchunk % BK != 0) return hipErrorInvalidValue;  // slices start on stage boundaries
     splits = cdiv(s.K, s.kchunk);
   }
+  if constexpr (EpiPersistent<Epi>::value && std::is_same<T, bf16_t>::value) {
+    if (splits == 1 && blocks > 2 * kLoopBlocks) {
+      hipLaunchKernelGGL((gemm_persistent_kernel<T, AK, BKM, Epi, Cfg>), dim3(kLoopBlocks), dim3(Cfg::THREADS), 0,
+                         stream, A, B, s, ep);
+      return hipGetLastError();
+    }
+  }
   hipLaunchKernelGGL((gemm_kernel<T, AK, BKM, Epi, Cfg>), dim3(static_cast<unsigned>(blocks), 1, splits),
                      dim3(Cfg::THREADS), 0, stream, A, B, s, ep);
   return hipGetLastError();
 }
 
-constexpr int kGatedBlocks = 256;  // one block per CU of a 256-CU GPU (a multiple of kNumXcd)
+constexpr int kGatedBlocks = kLoopBlocks;
 
 template <typename T, bool AK, bool BKM, class Epi, class Cfg>
 hipError_t launch_gemm_gated(Operand A, Operand B, GemmShape s, const typename Epi::Params &ep, const int *run_if,
