@@ -649,6 +649,26 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_pair_kerne
   }
 }
 
+// The pair as one block per CU looping over the same block order (logical
+// block t on block t mod gridDim.x, a multiple of 8), for two
+// weight-gradient products.
+template <typename T, bool AK1, bool BKM1, class Epi1, bool AK2, bool BKM2, class Epi2, class Cfg>
+__global__ __launch_bounds__(Cfg::THREADS, Cfg::MIN_BLOCKS) void gemm_pair_persistent_kernel(
+    Operand A1, Operand B1, GemmShape s1, typename Epi1::Params ep1, Operand A2, Operand B2, GemmShape s2,
+    typename Epi2::Params ep2, int blocks1, int base2, int total) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * Cfg::STAGE_BYTES];
+  const int tiles2 = cdiv(s2.M, Cfg::BM) * cdiv(s2.N, Cfg::BN);
+  for (int t = blockIdx.x; t < total; t += gridDim.x) {
+    if (t < blocks1) {
+      gemm_block<T, AK1, BKM1, Epi1, Cfg, true>(A1, B1, s1, ep1, t, blocks1, 0, smem);
+    } else if (t >= base2) {
+      const int b2 = t - base2;
+      gemm_block<T, AK2, BKM2, Epi2, Cfg, true>(A2, B2, s2, ep2, b2 % tiles2, tiles2, b2 / tiles2, smem);
+    }
+    __syncthreads();  // the next tile's first stage overwrites what the epilogue used
+  }
+}
+
 // Shapes the loaders handle.
 template <typename T, bool AK, bool BKM>
 bool gemm_shape_ok(const Operand &A, const Operand &B, const GemmShape &s) {
@@ -713,6 +733,14 @@ hipError_t launch_gemm_pair(Operand A1, Operand B1, GemmShape s1, const typename
     splits2 = cdiv(s2.K, s2.kchunk);
   }
   const int64_t base2 = (b1 + kNumXcd - 1) / kNumXcd * kNumXcd;
+  if constexpr (EpiPersistent<Epi1>::value && EpiPersistent<Epi2>::value && std::is_same<T, bf16_t>::value) {
+    if (base2 + b2 * splits2 > 2 * kLoopBlocks) {
+      hipLaunchKernelGGL((gemm_pair_persistent_kernel<T, AK1, BKM1, Epi1, AK2, BKM2, Epi2, Cfg>), dim3(kLoopBlocks),
+                         dim3(Cfg::THREADS), 0, stream, A1, B1, s1, ep1, A2, B2, s2, ep2, static_cast<int>(b1),
+                         static_cast<int>(base2), static_cast<int>(base2 + b2 * splits2));
+      return hipGetLastError();
+    }
+  }
   hipLaunchKernelGGL((gemm_pair_kernel<T, AK1, BKM1, Epi1, AK2, BKM2, Epi2, Cfg>),
                      dim3(static_cast<unsigned>(base2 + b2 * splits2)), dim3(Cfg::THREADS), 0, stream, A1, B1, s1, ep1, A2,
                      B2, s2, ep2, static_cast<int>(b1), static_cast<int>(base2));
