@@ -33,10 +33,12 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # without a split-K tail).
 LABEL_KERNELS = {
     "logits + softmax partials": "gemm_kernel<unsigned short, true, true, ee::EpiLogits<",
-    "output-matrix gradient": "gemm_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
+    "output-matrix gradient": ("gemm_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
+                               "gemm_persistent_kernel<unsigned short, true, true, ee::EpiWeightGrad<"),
     "dZ": ("gemm_kernel<unsigned short, false, false, ee::EpiStoreF32<",
            "gemm_pair_kernel<unsigned short, false, false, ee::EpiStoreF32<"),
-    "gate and up gradients": "gemm_pair_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
+    "gate and up gradients": ("gemm_pair_kernel<unsigned short, true, true, ee::EpiWeightGrad<",
+                              "gemm_pair_persistent_kernel<unsigned short, true, true, ee::EpiWeightGrad<"),
     "gate and up projections + swiglu": "ee::EpiGateUp<",
     "down projection + residual": "ee::EpiResidual<",
     "dA + swiglu backward, down gradient": "ee::EpiSwiGLUBwd<",
