@@ -172,6 +172,12 @@ SMALL_CASES = [
     # one and over four (ragged) rows of tiles
     ("norm_stagger_ragged_vocab", W.EXIT_NORM, 64, 64, 767 * 256 + 200, 0, "bf16", False),
     ("norm_stagger_ragged_rows", W.EXIT_NORM, 1000, 64, 199 * 256 + 156, 0, "bf16", True),
+    # weight gradients launched as one block per CU looping over the tiles
+    # (more than 512 tiles): dW_out over 3 x 201 tiles, ragged in both
+    # dimensions; the gate and up gradients as one looping pair, 289 + 289
+    # tiles ragged in both dimensions, with the pair's padding blocks between
+    ("norm_loop_ragged", W.EXIT_NORM, 70, 576, 200 * 256 + 100, 0, "bf16", False),
+    ("mlp_loop_ragged", W.EXIT_MLP, 96, 4160, 300, 4160, "bf16", False),
 ]
 
 
