@@ -79,7 +79,7 @@ def mm(a, b):
     underflows to zero)."""
     a = np.asarray(a)
     b = np.asarray(b)
-    if a.size * (b.shape[-1] if b.ndim > 1 else 1) <= 1 << 26:
+    if a.size * (b.shape[-1] if b.ndim > 1 else 1) <= 1 << 28:
         return np.asarray(a, dtype=np.float64) @ np.asarray(b, dtype=np.float64)
     return (np.asarray(a, dtype=np.float32) @ np.asarray(b, dtype=np.float32)).astype(np.float64)
 
