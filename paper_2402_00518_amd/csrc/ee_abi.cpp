@@ -303,7 +303,7 @@ hipEvent_t prof_event() {
 char *at(void *ws, size_t off) { return static_cast<char *>(ws) + off; }
 float *atf(void *ws, size_t off) { return reinterpret_cast<float *>(at(ws, off)); }
 
-bool unshifted_form(const ee_exit &e) { return e.beta == nullptr && e.vocab >= 64; }
+bool unshifted_form(const ee_exit &e) { return e.vocab >= 64; }
 
 // Forward of one exit; see ee_head_forward_loss.
 ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, const float *token_w, int64_t n64,
@@ -317,9 +317,9 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
   // The first exit of a call clears the device error record in its first
   // kernel; every exit's first kernel clears its range-check flag.
   int *clear = first ? reinterpret_cast<int *>(at(ws, kFlagOff)) : nullptr;
-  // Exits without a bias take the unshifted form of the logits (P = exp(S));
-  // with a bias the seed also sums G's rows, so they keep the shifted form,
-  // and so does a vocabulary of less than one 64-id slice (where the seed
+  // Exits take the unshifted form of the logits (P = exp(S)), with a bias
+  // too (G's row sums for its gradient then come from one read of P'),
+  // except for a vocabulary of less than one 64-id slice (where the seed
   // costs nothing, and a single id keeps its loss exactly 0: exp(S - m) = 1).
   const bool unshifted = unshifted_form(e);
   int *fb = reinterpret_cast<int *>(at(ws, L.fb));
@@ -391,7 +391,10 @@ ee_status run_forward(const ee_exit &e, const void *x, const int32_t *targets, c
     EE_LAUNCH("operand scale (or seed, if out of range) and loss", s,
               ee::launch_seed_or_scale(f32, at(ws, L.P), at(ws, L.zht), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), atf(ws, L.coef),
                                        targets, n, ldn, h, V, L.vtile, fb, atf(ws, L.bsum), static_cast<int>(cdiv64(n, 32)), loss,
-                                       total, w_e, first, s));
+                                       total, w_e, first, s, bias ? atf(ws, L.gsp) : nullptr));
+    if (bias)
+      EE_LAUNCH("logit-gradient row sums (unshifted form)", s,
+                ee::launch_gsum_unshifted(f32, at(ws, L.P), atf(ws, L.coef), n, ldn, V, fb, atf(ws, L.gsp), s));
   } else {
     EE_LAUNCH("logit seed", s, ee::launch_seed(f32, at(ws, L.P), atf(ws, L.pm), atf(ws, L.lse), atf(ws, L.sn), targets, n, ldn, V, L.vtile,
                                                s, bias ? atf(ws, L.gsp) : nullptr));

@@ -634,7 +634,10 @@ constexpr int kSeedRows = 128;
 template <typename T>
 __device__ __forceinline__ void seed_block(int bx, int by, T *P, const float *part_m, const float *lse,
                                            const float *sn, const int32_t *targets, int n, int ldn, int vocab,
-                                           int vtile, float *gsum_part) {
+                                           int vtile, float *gsum_part, const float *coef = nullptr) {
+  // coef != NULL: only the row sums of G = diag(coef) P (the unshifted
+  // form's G, with P's target entries already shifted); P is not written.
+  const bool sums_only = coef != nullptr;
   __shared__ float red[kSeedRows][4];
   const int c0 = by * 2048 + threadIdx.x * 8;
   if (gsum_part == nullptr && c0 >= ldn) return;
@@ -646,9 +649,10 @@ __device__ __forceinline__ void seed_block(int bx, int by, T *P, const float *pa
   for (int e = 0; e < 8; ++e) {
     const int c = c0 + e;
     ok[e] = c < n;
-    s[e] = ok[e] ? sn[c] : 0.0f;
-    lz[e] = ok[e] ? lse[c] : 0.0f;
-    yy[e] = ok[e] ? targets[c] : -1;
+    s[e] = ok[e] && !sums_only ? sn[c] : 0.0f;
+    lz[e] = ok[e] && !sums_only ? lse[c] : 0.0f;
+    yy[e] = ok[e] && !sums_only ? targets[c] : -1;
+    if (sums_only) cf[e] = ok[e] ? coef[c] : 0.0f;
   }
   int tile = -1;
   const int cl = min(c0, ldn - 8);  // threads past ldn (kept for the row sums) re-read the last chunk
@@ -659,7 +663,7 @@ __device__ __forceinline__ void seed_block(int bx, int by, T *P, const float *pa
     const int v0 = vb + 16 * b;
     const int rows = min(16, vocab - v0);
     if (rows <= 0) break;  // uniform: past the vocabulary
-    if (v0 / vtile != tile) {
+    if (!sums_only && v0 / vtile != tile) {
       tile = v0 / vtile;
 #pragma unroll
       for (int e = 0; e < 8; ++e)
@@ -685,7 +689,7 @@ __device__ __forceinline__ void seed_block(int bx, int by, T *P, const float *pa
         g[e] = ok[e] ? p[e] * cf[e] - (yy[e] == v0 + r ? s[e] : 0.0f) : 0.0f;
         rsum[r] += g[e];
       }
-      if (r < rows && c0 < ldn) store_f32<8>(P + static_cast<int64_t>(v0 + r) * ldn + c0, g);
+      if (!sums_only && r < rows && c0 < ldn) store_f32<8>(P + static_cast<int64_t>(v0 + r) * ldn + c0, g);
     }
     // Row sums of G over this block's tokens (LayerNorm bias gradient):
     // fp32, fixed order.  A reduce-scatter over the wave leaves lane l with
@@ -979,12 +983,13 @@ template <typename T>
 __global__ __launch_bounds__(256) void seed_or_scale_kernel(T *P, T *x_hat_t, const float *part_m, const float *lse,
                                                             const float *sn, const float *coef,
                                                             const int32_t *targets, int n, int ldn, int h, int vocab,
-                                                            int vtile, const int *fallback, FinalLoss fl) {
+                                                            int vtile, const int *fallback, float *gsum_part,
+                                                            FinalLoss fl) {
   const int b = blockIdx.x;
   if (b == 0) final_loss_block(fl.block_sums, fl.blocks, n, fl.loss, fl.total, fl.w, fl.first);
   if (*fallback != 0) {
     const int sx = cdiv(vocab, kSeedRows), sy = cdiv(ldn, 2048);  // seed_chunks(ldn)
-    if (b < sx * sy) seed_block<T>(b % sx, b / sx, P, part_m, lse, sn, targets, n, ldn, vocab, vtile, nullptr);
+    if (b < sx * sy) seed_block<T>(b % sx, b / sx, P, part_m, lse, sn, targets, n, ldn, vocab, vtile, gsum_part);
   } else {
     const int cx = cdiv(ldn, 2048), cy = h / 8;
     if (b < cx * cy) scale_block<T>(b % cx, b / cx, x_hat_t, P, coef, lse, targets, n, ldn, vocab);
@@ -994,7 +999,8 @@ __global__ __launch_bounds__(256) void seed_or_scale_kernel(T *P, T *x_hat_t, co
 hipError_t launch_seed_or_scale(bool f32, void *P, void *x_hat_t, const float *part_m, const float *lse,
                                 const float *sn, const float *coef, const int32_t *targets, int n, int ldn, int h,
                                 int vocab, int vtile, const int *fallback, const float *block_sums, int loss_blocks,
-                                float *loss, float *total, float w, int first, hipStream_t stream) {
+                                float *loss, float *total, float w, int first, hipStream_t stream,
+                                float *gsum_part) {
   if (n <= 0) return hipSuccess;
   if (h % 8 != 0 || h < 64 || ldn % 8 != 0 || fallback == nullptr) return hipErrorInvalidValue;
   const int64_t blocks = std::max<int64_t>(static_cast<int64_t>(cdiv(vocab, kSeedRows)) * seed_chunks(ldn),
@@ -1002,8 +1008,30 @@ hipError_t launch_seed_or_scale(bool f32, void *P, void *x_hat_t, const float *p
   if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
   EE_DISPATCH(f32, hipLaunchKernelGGL(seed_or_scale_kernel<T>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
                                       stream, static_cast<T *>(P), static_cast<T *>(x_hat_t), part_m, lse, sn, coef,
-                                      targets, n, ldn, h, vocab, vtile, fallback,
+                                      targets, n, ldn, h, vocab, vtile, fallback, gsum_part,
                                       FinalLoss{block_sums, loss_blocks, loss, total, w, first}));
+  return hipGetLastError();
+}
+
+// Row sums of G = diag(coef) P' per 2048-token chunk (the seed's partials),
+// for the bias gradient of an exit in the unshifted form, after the operand
+// scale has shifted P's target entries; nothing if the exit fell back to
+// the shifted form, whose seed wrote them.
+template <typename T>
+__global__ __launch_bounds__(256) void gsum_unshifted_kernel(const T *P, const float *coef, int n, int ldn, int vocab,
+                                                             const int *fallback, float *gsum_part) {
+  if (*fallback != 0) return;  // the same word for every thread
+  seed_block<T>(blockIdx.x, blockIdx.y, const_cast<T *>(P), nullptr, nullptr, nullptr, nullptr, n, ldn, vocab, 1,
+                gsum_part, coef);
+}
+
+hipError_t launch_gsum_unshifted(bool f32, const void *P, const float *coef, int n, int ldn, int vocab,
+                                 const int *fallback, float *gsum_part, hipStream_t stream) {
+  if (n <= 0 || vocab <= 0) return hipSuccess;
+  if (ldn % 8 != 0 || coef == nullptr || fallback == nullptr || gsum_part == nullptr) return hipErrorInvalidValue;
+  const dim3 grid(cdiv(vocab, kSeedRows), seed_chunks(ldn));
+  EE_DISPATCH(f32, hipLaunchKernelGGL(gsum_unshifted_kernel<T>, grid, dim3(256), 0, stream, static_cast<const T *>(P),
+                                      coef, n, ldn, vocab, fallback, gsum_part));
   return hipGetLastError();
 }
 

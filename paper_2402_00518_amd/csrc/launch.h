@@ -96,15 +96,22 @@ hipError_t launch_seed(bool f32, void *P, const float *part_m, const float *lse,
                        float *gsum_part = nullptr);
 
 // After the unshifted cross-entropy reduce: if *fallback is set, the seed
-// (as launch_seed, no row sums); else the operand scale, x_hat_t[j][c] *=
-// coef[c] (c < n) and, at each token's target, P[y_c][c] -= exp(lse[c]), so
-// that P holds P' with G = diag(coef) P'.  x_hat_t [h][ldn], P [V][ldn],
-// element type `f32`.  The same launch also does launch_final_loss's work
-// (block_sums .. first).
+// (as launch_seed, with G's row sums into gsum_part if it is not NULL); else
+// the operand scale, x_hat_t[j][c] *= coef[c] (c < n) and, at each token's
+// target, P[y_c][c] -= exp(lse[c]), so that P holds P' with
+// G = diag(coef) P'.  x_hat_t [h][ldn], P [V][ldn], element type `f32`.
+// The same launch also does launch_final_loss's work (block_sums .. first).
 hipError_t launch_seed_or_scale(bool f32, void *P, void *x_hat_t, const float *part_m, const float *lse,
                                 const float *sn, const float *coef, const int32_t *targets, int n, int ldn, int h,
                                 int vocab, int vtile, const int *fallback, const float *block_sums, int blocks,
-                                float *loss, float *total, float w, int first, hipStream_t stream);
+                                float *loss, float *total, float w, int first, hipStream_t stream,
+                                float *gsum_part = nullptr);
+// After launch_seed_or_scale, for an exit with a bias: unless *fallback is
+// set (the seed wrote them), the row sums of G = diag(coef) P' per chunk of
+// 2048 tokens, gsum_part[chunk][v] = sum_{c in chunk, c < n} coef[c] P'[v][c],
+// as launch_seed's.
+hipError_t launch_gsum_unshifted(bool f32, const void *P, const float *coef, int n, int ldn, int vocab,
+                                 const int *fallback, float *gsum_part, hipStream_t stream);
 
 // loss[0] = sum(block_sums) / n;  total[0] = (first ? 0 : total[0]) + w * loss[0].
 hipError_t launch_final_loss(const float *block_sums, int blocks, int n, float *loss, float *total,

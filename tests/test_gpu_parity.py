@@ -406,18 +406,20 @@ def test_mlp_gate_and_up_in_one_buffer():
 # Embedding exits, and a ragged shape), and rows whose logits all lie far
 # below zero.
 FALLBACK_CASES = [
-    ("range_large_norm", W.EXIT_NORM, 300, 256, 1000, 0, "bf16"),
-    ("range_large_norm_ragged", W.EXIT_NORM, 130, 192, 700, 0, "bf16"),
-    ("range_large_mlp", W.EXIT_MLP, 260, 192, 900, 320, "bf16"),
-    ("range_large_embedding", W.EXIT_EMBEDDING, 200, 128, 600, 0, "bf16"),
-    ("range_large_f32", W.EXIT_NORM, 150, 128, 300, 0, "f32"),
+    ("range_large_norm", W.EXIT_NORM, 300, 256, 1000, 0, "bf16", "rms", False),
+    ("range_large_norm_ragged", W.EXIT_NORM, 130, 192, 700, 0, "bf16", "rms", False),
+    ("range_large_mlp", W.EXIT_MLP, 260, 192, 900, 320, "bf16", "rms", False),
+    ("range_large_embedding", W.EXIT_EMBEDDING, 200, 128, 600, 0, "bf16", "rms", False),
+    ("range_large_f32", W.EXIT_NORM, 150, 128, 300, 0, "f32", "rms", False),
+    # a bias: the seed of the shifted rerun also sums G's rows
+    ("range_large_layernorm_bias", W.EXIT_NORM, 300, 256, 1000, 0, "bf16", "layer", True),
 ]
 
 
-@pytest.mark.parametrize("name,kind,n,h,v,inter,dtype", FALLBACK_CASES, ids=[c[0] for c in FALLBACK_CASES])
-def test_logits_out_of_the_unshifted_range(name, kind, n, h, v, inter, dtype):
+@pytest.mark.parametrize("name,kind,n,h,v,inter,dtype,norm,bias", FALLBACK_CASES, ids=[c[0] for c in FALLBACK_CASES])
+def test_logits_out_of_the_unshifted_range(name, kind, n, h, v, inter, dtype, norm, bias):
     say(f"case: {name} (logits scaled past the unshifted range)")
-    b = small(kind, n, h, v, inter, dtype, seed=71, name=name)
+    b = small(kind, n, h, v, inter, dtype, seed=71, name=name, norm=norm, bias=bias)
     ex = b.exits[0]
     w = W.decode(ex.w_out)
     # rows of Z have norm about sqrt(h) (Embedding: the raw hidden rows);
