@@ -67,7 +67,9 @@ def side_pass_bytes(w, name):
     the rows, write their scales, Z and the token-contiguous copy of x_hat, or
     U and the token-contiguous copy of U_hat; norm statistics: read the rows;
     norm apply: read the rows and the scales, write as the one pass does;
-    cross-entropy reduce: read the softmax partials;
+    cross-entropy reduce: read the softmax partials; G's row sums (a bias
+    in the unshifted form): read P' and the coefficients, write the
+    per-chunk sums;
     seed: read P and write G in place; operand scale: read and write the
     token-contiguous x_hat, read the per-token coefficients)."""
     N, h, V, I = w.n_tokens, w.hidden, w.vocab, w.intermediate
@@ -84,6 +86,7 @@ def side_pass_bytes(w, name):
         "cross-entropy reduce": 2 * slices * ldn * 4 + 3 * N * 4,
         "logit seed": 2 * V * ldn * es + slices * ldn * 4,
         "operand scale (or seed, if out of range) and loss": 2 * h * ldn * es + 2 * N * 4,
+        "logit-gradient row sums (unshifted form)": V * ldn * es + ldn * 4 + ((ldn + 2047) // 2048) * V * 4,
         "exit norm backward": 2 * N * h * 4 + N * h * es,
     }
     return table.get(name)

@@ -29,7 +29,7 @@ and accumulation, fp32 weight gradients):
 The rounding points follow the precision convention of the boundary
 (norms, softmax and losses in fp32; GEMMs on bf16 operands with fp32
 accumulation; the logits stored once in bf16 as exp(S - m) and turned into
-the bf16 logit-gradient seed G, or, for exits without a bias, stored as
+the bf16 logit-gradient seed G, or, in the unshifted form, stored as
 exp(S) with the per-token factor s_n exp(-LSE_n) rounded into the bf16
 token-contiguous x_hat and the target entries shifted by exp(LSE_n) in
 bf16; weight gradients in fp32).  Both forms round each term P x_hat of a
